@@ -1,0 +1,295 @@
+// C ABI of the library (declared in include/vc_attn.h): argument validation on the host, the
+// workspace carve-up, and the launches of the preprocessing, grouping and attention kernels.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "vc_attn.h"
+#include "vc_internal.hpp"
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+constexpr int kD = 128;
+constexpr int kKMax = 64;
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline int blocks_of(int n, int b) { return (n + b - 1) / b; }
+
+vc_status check_shape(const vc_shape* s) {
+  if (!s) return VC_ERR_NULL;
+  if (s->d != kD || s->B < 1 || s->H < 1 || s->N < 1 || s->F < 1 || s->Ht < 1 || s->Wd < 1) return VC_ERR_SHAPE;
+  if ((long long)s->F * s->Ht * s->Wd != s->N) return VC_ERR_SHAPE;
+  const long long T = blocks_of(s->N, 128);
+  if ((long long)s->B * s->H * T * 128 * kD >= (1LL << 31)) return VC_ERR_SHAPE;
+  return VC_OK;
+}
+
+vc_status check_opts(const vc_opts* o) {
+  if (!o) return VC_ERR_NULL;
+  if (o->qk_fmt != VC_QK_INT8) return VC_ERR_UNSUPPORTED;
+  if (o->p_mode != VC_P_EXPCAST && o->p_mode != VC_P_EXP_THEN_CAST) return VC_ERR_UNSUPPORTED;
+  const int32_t flags[4] = {o->rope, o->hadamard, o->smooth_k, o->smooth_v};
+  for (int32_t f : flags)
+    if (f != 0 && f != 1) return VC_ERR_UNSUPPORTED;
+  if (!std::isfinite(o->sm_scale) || o->sm_scale < 0.f || !std::isfinite(o->beta)) return VC_ERR_UNSUPPORTED;
+  return VC_OK;
+}
+
+vc_status check_group_opts(const vc_shape* s, const vc_group_opts* g) {
+  if (!g) return VC_ERR_NULL;
+  if (g->mode == VC_GROUP_IDENTITY) return VC_OK;
+  if (g->mode == VC_GROUP_CUBE) {
+    if (g->cube[0] < 1 || g->cube[1] < 1 || g->cube[2] < 1) return VC_ERR_UNSUPPORTED;
+    return VC_OK;
+  }
+  if (g->mode != VC_GROUP_KMEANS) return VC_ERR_UNSUPPORTED;
+  if (g->k < 1 || g->k > kKMax || g->k > s->N) return VC_ERR_UNSUPPORTED;
+  if (g->iters < 0 || g->iters > 64 || (g->warm_start != 0 && g->warm_start != 1)) return VC_ERR_UNSUPPORTED;
+  return VC_OK;
+}
+
+size_t prep_ws(const vc_shape* s) {
+  const size_t BH = (size_t)s->B * s->H, T = blocks_of(s->N, 128);
+  return 2 * align256(BH * T * kD * 4) + align256(BH * kD * 4);
+}
+
+size_t group_ws(const vc_shape* s, const vc_group_opts* g) {
+  if (g->mode != VC_GROUP_KMEANS) return 0;
+  const size_t BH = (size_t)s->B * s->H, N = s->N, K = g->k, nblk = blocks_of(s->N, 256);
+  return align256(BH * N * kD) + align256(BH * 4) + align256(BH * K * kD * 4) + align256(BH * nblk * K * kD * 4) +
+         2 * align256(BH * nblk * K * 4);
+}
+
+vc_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return VC_OK;
+  g_last_hip = (int)e;
+  return VC_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+void vc_opts_default(vc_opts* o) {
+  if (!o) return;
+  o->qk_fmt = VC_QK_INT8;
+  o->p_mode = VC_P_EXPCAST;
+  o->rope = o->hadamard = o->smooth_k = o->smooth_v = 1;
+  o->sm_scale = 0.f;
+  o->beta = -0.35f;
+}
+
+void vc_group_opts_default(vc_group_opts* g) {
+  if (!g) return;
+  g->mode = VC_GROUP_KMEANS;
+  g->k = 32;
+  g->iters = 8;
+  g->warm_start = 0;
+  g->cube[0] = 4;
+  g->cube[1] = 2;
+  g->cube[2] = 16;
+}
+
+size_t vc_attn_workspace_size(const vc_shape* shape, const vc_opts* opts, const vc_group_opts* gopts) {
+  if (check_shape(shape) != VC_OK) return 0;
+  size_t ws = 0;
+  if (opts) {
+    if (check_opts(opts) != VC_OK) return 0;
+    ws = prep_ws(shape);
+  }
+  if (gopts) {
+    if (check_group_opts(shape, gopts) != VC_OK) return 0;
+    const size_t g = group_ws(shape, gopts);
+    ws = ws > g ? ws : g;
+  }
+  return ws;
+}
+
+vc_status vc_rope_tables(int32_t F, int32_t Ht, int32_t Wd, double theta, float* cos_t, float* sin_t) {
+  if (!cos_t || !sin_t) return VC_ERR_NULL;
+  if (F < 1 || Ht < 1 || Wd < 1 || !(theta > 0.0)) return VC_ERR_SHAPE;
+  const int rows = F + Ht + Wd;
+  for (int r = 0; r < rows; ++r) {
+    const int axis = r < F ? 0 : (r < F + Ht ? 1 : 2);
+    const int pos = axis == 0 ? r : (axis == 1 ? r - F : r - F - Ht);
+    const int first = axis == 0 ? 0 : (axis == 1 ? 22 : 43);
+    const int npair = axis == 0 ? 22 : 21;
+    const double dims = axis == 0 ? 44.0 : 42.0;
+    for (int i = 0; i < 64; ++i) {
+      const int j = i - first;
+      if (j < 0 || j >= npair) {
+        cos_t[r * 64 + i] = 1.0f;
+        sin_t[r * 64 + i] = 0.0f;
+        continue;
+      }
+      const double ang = (double)pos * std::pow(theta, -(2.0 * j) / dims);
+      cos_t[r * 64 + i] = (float)std::cos(ang);
+      sin_t[r * 64 + i] = (float)std::sin(ang);
+    }
+  }
+  return VC_OK;
+}
+
+vc_status vc_attn_group(const vc_shape* shape, const vc_group_opts* gopts, const uint16_t* V, float* centroids,
+                        int32_t* labels, int32_t* perm, int32_t* inv_perm, void* ws, size_t ws_bytes, void* stream) {
+  vc_status st = check_shape(shape);
+  if (st != VC_OK) return st;
+  if ((st = check_group_opts(shape, gopts)) != VC_OK) return st;
+  if (!labels || !perm) return VC_ERR_NULL;
+  const bool km = gopts->mode == VC_GROUP_KMEANS;
+  if (km && (!V || !centroids)) return VC_ERR_NULL;
+  const size_t need = group_ws(shape, gopts);
+  if (need > 0 && (!ws || ws_bytes < need)) return VC_ERR_WORKSPACE;
+  if ((V && !aligned16(V)) || !aligned16(labels) || !aligned16(perm) || (inv_perm && !aligned16(inv_perm)) ||
+      (centroids && !aligned16(centroids)) || (ws && !aligned16(ws)))
+    return VC_ERR_ALIGN;
+
+  vc::GroupArgs a{};
+  const size_t BH = (size_t)shape->B * shape->H;
+  a.V = V;
+  a.centroids = centroids;
+  a.labels = labels;
+  a.perm = perm;
+  a.inv_perm = inv_perm;
+  a.N = shape->N;
+  a.F = shape->F;
+  a.Ht = shape->Ht;
+  a.Wd = shape->Wd;
+  a.mode = gopts->mode;
+  a.k = km ? gopts->k : 1;
+  a.iters = gopts->iters;
+  a.warm_start = gopts->warm_start;
+  a.cube_t = gopts->cube[0];
+  a.cube_h = gopts->cube[1];
+  a.cube_w = gopts->cube[2];
+  a.nblk = blocks_of(shape->N, 256);
+  a.nlab = a.k;
+  if (km) {
+    char* p = static_cast<char*>(ws);
+    const size_t N = shape->N, K = a.k, nblk = a.nblk;
+    a.codes = reinterpret_cast<int8_t*>(p);
+    p += align256(BH * N * kD);
+    a.scale = reinterpret_cast<float*>(p);
+    p += align256(BH * 4);
+    a.cent = reinterpret_cast<int32_t*>(p);
+    p += align256(BH * K * kD * 4);
+    a.sums = reinterpret_cast<int32_t*>(p);
+    p += align256(BH * nblk * K * kD * 4);
+    a.counts = reinterpret_cast<int32_t*>(p);
+    p += align256(BH * nblk * K * 4);
+    a.blockhist = reinterpret_cast<int32_t*>(p);
+  }
+  return hip_status(vc::launch_group(a, (int)BH, static_cast<hipStream_t>(stream)));
+}
+
+vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_t* Q, const uint16_t* K,
+                       const uint16_t* V, const int32_t* perm, const int32_t* q_perm, const float* rope_cos,
+                       const float* rope_sin, const vc_prepped* out, void* ws, size_t ws_bytes, void* stream) {
+  vc_status st = check_shape(shape);
+  if (st != VC_OK) return st;
+  if ((st = check_opts(opts)) != VC_OK) return st;
+  if (!Q || !K || !V || !out) return VC_ERR_NULL;
+  if (!out->q || !out->q_scale || !out->k || !out->k_scale || !out->k_mean || !out->v || !out->v_scale ||
+      !out->v_mean)
+    return VC_ERR_NULL;
+  if (opts->rope && (!rope_cos || !rope_sin)) return VC_ERR_NULL;
+  if (!ws || ws_bytes < prep_ws(shape)) return VC_ERR_WORKSPACE;
+  const void* ptrs[] = {Q, K, V, out->q, out->q_scale, out->k, out->k_scale, out->k_mean, out->v, out->v_scale,
+                        out->v_mean, ws};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return VC_ERR_ALIGN;
+  if ((perm && !aligned16(perm)) || (q_perm && !aligned16(q_perm)) || (rope_cos && !aligned16(rope_cos)) ||
+      (rope_sin && !aligned16(rope_sin)))
+    return VC_ERR_ALIGN;
+
+  vc::PrepArgs a{};
+  const size_t BH = (size_t)shape->B * shape->H, T = blocks_of(shape->N, 128);
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.perm = perm;
+  a.q_perm = q_perm;
+  a.rope_cos = rope_cos;
+  a.rope_sin = rope_sin;
+  a.q = out->q;
+  a.q_scale = out->q_scale;
+  a.k = out->k;
+  a.k_scale = out->k_scale;
+  a.k_mean = out->k_mean;
+  a.v = out->v;
+  a.v_scale = out->v_scale;
+  a.v_mean = out->v_mean;
+  char* p = static_cast<char*>(ws);
+  a.ws_ksum = reinterpret_cast<float*>(p);
+  p += align256(BH * T * kD * 4);
+  a.ws_vamax = reinterpret_cast<float*>(p);
+  p += align256(BH * T * kD * 4);
+  a.ws_vinv = reinterpret_cast<float*>(p);
+  a.N = shape->N;
+  a.T = (int)T;
+  a.F = shape->F;
+  a.Ht = shape->Ht;
+  a.Wd = shape->Wd;
+  a.rope = opts->rope;
+  a.hadamard = opts->hadamard;
+  a.smooth_k = opts->smooth_k;
+  a.smooth_v = opts->smooth_v;
+  return hip_status(vc::launch_prep(a, (int)BH, static_cast<hipStream_t>(stream)));
+}
+
+vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in, const int32_t* q_perm,
+                          uint16_t* O, void* stream) {
+  vc_status st = check_shape(shape);
+  if (st != VC_OK) return st;
+  if ((st = check_opts(opts)) != VC_OK) return st;
+  if (!in || !O) return VC_ERR_NULL;
+  if (!in->q || !in->q_scale || !in->k || !in->k_scale || !in->v || !in->v_scale || !in->v_mean) return VC_ERR_NULL;
+  const void* ptrs[] = {in->q, in->q_scale, in->k, in->k_scale, in->v, in->v_scale, in->v_mean, O};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return VC_ERR_ALIGN;
+  if (q_perm && !aligned16(q_perm)) return VC_ERR_ALIGN;
+
+  vc::FwdArgs a{};
+  const size_t BH = (size_t)shape->B * shape->H;
+  a.q = in->q;
+  a.q_scale = in->q_scale;
+  a.k = in->k;
+  a.k_scale = in->k_scale;
+  a.v = in->v;
+  a.v_scale = in->v_scale;
+  a.v_mean = in->v_mean;
+  a.q_perm = q_perm;
+  a.O = O;
+  a.N = shape->N;
+  a.T = blocks_of(shape->N, 128);
+  // score scale in log2 units: sm_scale * log2(e), with the unnormalised Hadamard's 1/128
+  const double sm = opts->sm_scale > 0.f ? (double)opts->sm_scale : (double)(float)(1.0 / std::sqrt(128.0));
+  double kappa = sm * 1.4426950408889634074;
+  if (opts->hadamard) kappa /= 128.0;
+  a.kappa = (float)kappa;
+  a.cbias = 120.0f + opts->beta;
+  a.p_mode = opts->p_mode;
+  a.smooth_v = opts->smooth_v;
+  return hip_status(vc::launch_forward(a, (int)BH, static_cast<hipStream_t>(stream)));
+}
+
+const char* vc_status_str(vc_status s) {
+  switch (s) {
+    case VC_OK: return "ok";
+    case VC_ERR_NULL: return "a required pointer is NULL";
+    case VC_ERR_SHAPE: return "unsupported shape (d must be 128, N = F*Ht*Wd, sizes positive and bounded)";
+    case VC_ERR_UNSUPPORTED: return "unsupported option value";
+    case VC_ERR_WORKSPACE: return "workspace missing or too small";
+    case VC_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
+    case VC_ERR_HIP: return "HIP launch or runtime error";
+    case VC_ERR_INTERNAL: return "internal error";
+  }
+  return "unknown status";
+}
+
+int vc_last_hip_error(void) { return g_last_hip; }
+
+}  // extern "C"

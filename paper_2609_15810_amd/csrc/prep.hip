@@ -1,0 +1,321 @@
+// Fused preprocessing of the 8-bit VC-Attention operands (Sec. 3.4 and Appendix B).
+//
+// Three launches per call:
+//   prep_stats    grid (T, B*H), 128 threads. Wave 0: rotated key rows of original-order block
+//                 j summed per channel (the centering statistics). Wave 1: value rows of
+//                 permuted block j (gathered by perm): the block mean mu_j, stored as bf16, and
+//                 the per-channel max |V' - mu_j| of the block.
+//   prep_finalize grid (B*H), 128 threads: key channel mean and per-channel value scale.
+//   prep_quant    grid (T, B*H, 3), 256 threads. z = 0: Q rows (RoPE, Hadamard, per-block
+//                 INT8); z = 1: K' rows (gather, RoPE, centering, Hadamard, per-block INT8);
+//                 z = 2: V' rows (gather, demean, per-channel E4M3), transposed into the tile
+//                 order of the attention kernel.
+// All floating-point steps that decide a stored code are written as single IEEE fp32
+// operations in a fixed order (compiled with -ffp-contract=off; fused multiply-adds are spelled
+// out), so the codes, scales and means are reproducible bit for bit.
+#include "vc_common.hpp"
+#include "vc_internal.hpp"
+
+namespace vc {
+
+// One rotary pair at token n: y0 = fma(x0, c, -(x1 s)), y1 = fma(x0, s, x1 c).
+__device__ __forceinline__ void rope_pair(float& x0, float& x1, int pair, int n, const PrepArgs& a) {
+  const int x = n % a.Wd, y = (n / a.Wd) % a.Ht, f = n / (a.Wd * a.Ht);
+  const int ax = rope_axis(pair);
+  const int row = ax == 0 ? f : (ax == 1 ? a.F + y : a.F + a.Ht + x);
+  const float c = a.rope_cos[row * 64 + pair], s = a.rope_sin[row * 64 + pair];
+  const float p = x1 * s, q = x1 * c;
+  const float y0 = __builtin_fmaf(x0, c, -p);
+  const float y1 = __builtin_fmaf(x0, s, q);
+  x0 = y0;
+  x1 = y1;
+}
+
+// ------------------------------------------------------------------------------------------
+// Statistics: per-block key channel sums and value block means / residual maxima.
+// Lane p of a wave owns channels (2p, 2p+1) and walks the block's rows in ascending order, so
+// every per-channel sum is a sequential fp32 sum from 0.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(128) void prep_stats(PrepArgs a) {
+  __shared__ uint32_t vrows[BLK][64];  // the block's gathered value rows, for the second pass
+  const int j = blockIdx.x, bh = blockIdx.y;
+  const int wave = threadIdx.x >> 6, p = threadIdx.x & 63;
+  const int r0 = j * BLK;
+  const int valid = min(BLK, a.N - r0);
+  const size_t head = (size_t)bh * a.N;
+
+  if (wave == 0) {
+    if (!a.smooth_k) return;
+    const uint32_t* K = reinterpret_cast<const uint32_t*>(a.K) + head * 64 + p;
+    float s0 = 0.f, s1 = 0.f;
+    for (int r = 0; r < valid; r += 8) {
+      uint32_t w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) w[u] = (r + u < valid) ? K[(size_t)(r0 + r + u) * 64] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (r + u < valid) {
+          float x0 = bf16_lo(w[u]), x1 = bf16_hi(w[u]);
+          if (a.rope) rope_pair(x0, x1, p, r0 + r + u, a);
+          s0 = s0 + x0;
+          s1 = s1 + x1;
+        }
+      }
+    }
+    float* out = a.ws_ksum + ((size_t)bh * a.T + j) * D + 2 * p;
+    out[0] = s0;
+    out[1] = s1;
+  } else {
+    const uint32_t* V = reinterpret_cast<const uint32_t*>(a.V) + head * 64 + p;
+    const int32_t* perm = a.perm ? a.perm + head : nullptr;
+    float s0 = 0.f, s1 = 0.f;
+    for (int r = 0; r < valid; r += 8) {
+      uint32_t w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int row = r0 + r + u;
+        const int n = perm ? clamp_index(perm[min(row, a.N - 1)], a.N) : row;
+        w[u] = (r + u < valid) ? V[(size_t)n * 64] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (r + u < valid) {
+          vrows[r + u][p] = w[u];
+          s0 = s0 + bf16_lo(w[u]);
+          s1 = s1 + bf16_hi(w[u]);
+        }
+      }
+    }
+    float mu0 = 0.f, mu1 = 0.f;
+    uint16_t* mean_out = a.v_mean + ((size_t)bh * a.T + j) * D + 2 * p;
+    if (a.smooth_v) {
+      const uint16_t b0 = f32_to_bf16(s0 / (float)valid), b1 = f32_to_bf16(s1 / (float)valid);
+      mean_out[0] = b0;
+      mean_out[1] = b1;
+      mu0 = bf16_to_f32(b0);
+      mu1 = bf16_to_f32(b1);
+    } else {
+      mean_out[0] = 0;
+      mean_out[1] = 0;
+    }
+    float m0 = 0.f, m1 = 0.f;
+    for (int r = 0; r < valid; ++r) {  // same wave wrote vrows: no barrier needed
+      const uint32_t w = vrows[r][p];
+      m0 = fmaxf(m0, fabsf(bf16_lo(w) - mu0));
+      m1 = fmaxf(m1, fabsf(bf16_hi(w) - mu1));
+    }
+    float* out = a.ws_vamax + ((size_t)bh * a.T + j) * D + 2 * p;
+    out[0] = m0;
+    out[1] = m1;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Finalize: key channel mean (sequential sum of the block sums, one division by N) and the
+// per-channel residual scale amax/448 with its reciprocal 448/amax.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(128) void prep_finalize(PrepArgs a) {
+  const int bh = blockIdx.x, c = threadIdx.x;
+  float km = 0.f;
+  if (a.smooth_k) {
+    const float* part = a.ws_ksum + (size_t)bh * a.T * D + c;
+    float tot = 0.f;
+    for (int j = 0; j < a.T; ++j) tot = tot + part[(size_t)j * D];
+    km = tot / (float)a.N;
+  }
+  a.k_mean[(size_t)bh * D + c] = km;
+  const float* am = a.ws_vamax + (size_t)bh * a.T * D + c;
+  float amax = 0.f;
+  for (int j = 0; j < a.T; ++j) amax = fmaxf(amax, am[(size_t)j * D]);
+  a.v_scale[(size_t)bh * D + c] = amax > 0.f ? amax / 448.f : 1.f;
+  a.ws_vinv[(size_t)bh * D + c] = amax > 0.f ? 448.f / amax : 0.f;
+}
+
+// ------------------------------------------------------------------------------------------
+// Quantization. A 128-row block per workgroup; 4 lanes per row, lane k4 = lane & 3 holding the
+// 32 channels c = 32 i + 8 k4 + e (i, e = 0..3, 0..7): the loads are 16-byte row segments and
+// the 128-point Walsh-Hadamard transform needs only two cross-lane stages (channel bits 3, 4).
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Butterfly stage h (channel bit b): lo <- lo + hi, hi <- lo - hi, in the order of the oracle.
+__device__ __forceinline__ void fwht_rows(float (&x)[4][8], int k4) {
+  // bits 0..2: e, inside the lane
+#pragma unroll
+  for (int h = 1; h < 8; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if ((e & h) == 0) {
+          const float lo = x[i][e], hi = x[i][e + h];
+          x[i][e] = lo + hi;
+          x[i][e + h] = lo - hi;
+        }
+  // bits 3, 4: k4, across lanes (xor 1, xor 2)
+#pragma unroll
+  for (int m = 1; m <= 2; m <<= 1) {
+    const bool upper = (k4 & m) != 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float own = x[i][e], other = __shfl_xor(own, m);
+        x[i][e] = upper ? other - own : own + other;
+      }
+  }
+  // bits 5, 6: i, inside the lane
+#pragma unroll
+  for (int h = 1; h < 4; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if ((i & h) == 0)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float lo = x[i][e], hi = x[i + h][e];
+          x[i][e] = lo + hi;
+          x[i + h][e] = lo - hi;
+        }
+}
+
+__device__ __forceinline__ void load_row32(const uint16_t* row, int k4, float (&x)[4][8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const u4 w = *reinterpret_cast<const u4*>(row + 32 * i + 8 * k4);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[i][2 * q] = bf16_lo(w[q]);
+      x[i][2 * q + 1] = bf16_hi(w[q]);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void prep_quant(PrepArgs a) {
+  __shared__ float red[4];
+  __shared__ uint8_t vt[BLK][D + 8];  // V codes of the block, row-major (8-byte rows), for the transpose
+  const int j = blockIdx.x, bh = blockIdx.y, z = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, k4 = lane & 3;
+  const int r0 = j * BLK;
+  const size_t head = (size_t)bh * a.N;
+  const uint16_t* X = z == 0 ? a.Q : (z == 1 ? a.K : a.V);
+  const int32_t* gather = z == 0 ? (a.q_perm ? a.q_perm + head : nullptr) : (a.perm ? a.perm + head : nullptr);
+
+  float x[2][4][8];
+  bool valid[2];
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int rl = wave * 32 + it * 16 + (lane >> 2);
+    const int row = r0 + rl;
+    valid[it] = row < a.N;
+    const int n = valid[it] ? (gather ? clamp_index(gather[row], a.N) : row) : 0;
+    load_row32(X + (head + n) * D, k4, x[it]);
+    if (z < 2) {
+      if (a.rope)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) rope_pair(x[it][i][e], x[it][i][e + 1], 16 * i + 4 * k4 + e / 2, n, a);
+      if (z == 1 && a.smooth_k) {
+        const float* km = a.k_mean + (size_t)bh * D;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[it][i][e] = x[it][i][e] - km[32 * i + 8 * k4 + e];
+      }
+      if (a.hadamard) fwht_rows(x[it], k4);
+    }
+    if (!valid[it])
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[it][i][e] = 0.f;
+  }
+
+  if (z < 2) {
+    // per-block symmetric INT8: scale = amax/127, code = rint(x * (127/amax))
+    float m = 0.f;
+#pragma unroll
+    for (int it = 0; it < 2; ++it)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(x[it][i][e]));
+    m = wave_max(m);
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float inv = amax > 0.f ? 127.f / amax : 0.f;
+    int8_t* codes = (z == 0 ? a.q : a.k) + ((size_t)bh * a.T + j) * (BLK * D);
+    if (threadIdx.x == 0) (z == 0 ? a.q_scale : a.k_scale)[(size_t)bh * a.T + j] = amax > 0.f ? amax / 127.f : 1.f;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int rl = wave * 32 + it * 16 + (lane >> 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float q = __builtin_rintf(x[it][i][e] * inv);
+          q = fminf(fmaxf(q, -127.f), 127.f);
+          const uint32_t b = (uint32_t)((int)q & 0xff);
+          if (e < 4) lo |= b << (8 * e); else hi |= b << (8 * (e - 4));
+        }
+        *reinterpret_cast<uint2*>(codes + qk_tile_offset(rl, 32 * i + 8 * k4)) = make_uint2(lo, hi);
+      }
+    }
+  } else {
+    // V': subtract the block mean (bf16, written by prep_stats), scale per channel, E4M3 RNE
+    const uint16_t* mu = a.v_mean + ((size_t)bh * a.T + j) * D;
+    const float* vinv = a.ws_vinv + (size_t)bh * D;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int rl = wave * 32 + it * 16 + (lane >> 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t w2[2] = {0u, 0u};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const int c = 32 * i + 8 * k4 + e;
+          const float m0 = a.smooth_v ? bf16_to_f32(mu[c]) : 0.f, m1 = a.smooth_v ? bf16_to_f32(mu[c + 1]) : 0.f;
+          // a channel whose residual is identically zero has vinv = 0 and stores +0
+          const float i0 = vinv[c], i1 = vinv[c + 1];
+          const float y0 = i0 != 0.f ? (x[it][i][e] - m0) * i0 : 0.f;
+          const float y1 = i1 != 0.f ? (x[it][i][e + 1] - m1) * i1 : 0.f;
+          uint32_t pk = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false) & 0xffffu;
+          if (!valid[it]) pk = 0;
+          w2[e >> 2] |= pk << (16 * ((e >> 1) & 1));
+        }
+        *reinterpret_cast<uint2*>(&vt[rl][32 * i + 8 * k4]) = make_uint2(w2[0], w2[1]);
+      }
+    }
+    __syncthreads();
+    // transposed store: 1024 chunks of 16 bytes, 4 per thread; chunk = (kc, db, kh, sh, c)
+    uint8_t* codes = a.v + ((size_t)bh * a.T + j) * (BLK * D);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int chunk = threadIdx.x + 256 * u;
+      const int c = chunk & 31, sh = (chunk >> 5) & 1, kh = (chunk >> 6) & 1, db = (chunk >> 7) & 3, kc = chunk >> 9;
+      const int ch = 32 * db + c;
+      uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const int key = 32 * (2 * kc + sh) + 8 * (t >> 2) + 4 * kh + (t & 3);
+        w[t >> 2] |= (uint32_t)vt[key][ch] << (8 * (t & 3));
+      }
+      *reinterpret_cast<u4*>(codes + (size_t)chunk * 16) = u4{w[0], w[1], w[2], w[3]};
+    }
+  }
+}
+
+hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
+  prep_stats<<<dim3(a.T, BH), 128, 0, s>>>(a);
+  prep_finalize<<<dim3(BH), 128, 0, s>>>(a);
+  prep_quant<<<dim3(a.T, BH, 3), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace vc

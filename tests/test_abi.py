@@ -1,0 +1,131 @@
+"""The C ABI: the library loads without a GPU, exports every entry point the header declares,
+and rejects invalid arguments on the host before anything is launched."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_15810_amd as vc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(vc.LIB_PATH):
+        from paper_2609_15810_amd import build
+        build.build()
+    return vc.lib()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "vc_attn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vc_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert {"vc_attn_group", "vc_attn_prep", "vc_attn_forward", "vc_attn_workspace_size",
+            "vc_status_str", "vc_last_hip_error", "vc_rope_tables"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings(L):
+    for s in range(8):
+        assert len(L.vc_status_str(s)) > 0
+
+
+def shape(**kw):
+    s = vc.make_shape(1, 2, (4, 16, 16))
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def prep_call(L, s, o, ptrs=None, ws_bytes=1 << 30, rope=True):
+    P = vc.Prepped(*([FAKE] * 8)) if ptrs is None else ptrs
+    return L.vc_attn_prep(C.byref(s), C.byref(o), FAKE, FAKE, FAKE, None, None, FAKE if rope else None,
+                          FAKE if rope else None, C.byref(P), FAKE, ws_bytes, None)
+
+
+def test_prep_validation(L):
+    o = vc.make_opts()
+    assert prep_call(L, shape(d=64), o) == 2
+    assert prep_call(L, shape(N=1000), o) == 2
+    assert prep_call(L, shape(B=0), o) == 2
+    bad = vc.make_opts(); bad.p_mode = 7
+    assert prep_call(L, shape(), bad) == 3
+    bad = vc.make_opts(); bad.smooth_v = 2
+    assert prep_call(L, shape(), bad) == 3
+    bad = vc.make_opts(); bad.qk_fmt = 1
+    assert prep_call(L, shape(), bad) == 3
+    assert prep_call(L, shape(), o, ws_bytes=16) == 4
+    P = vc.Prepped(*([FAKE] * 8)); P.v_mean = None
+    assert prep_call(L, shape(), o, ptrs=P) == 1
+    P = vc.Prepped(*([FAKE] * 8)); P.k = FAKE + 4
+    assert prep_call(L, shape(), o, ptrs=P) == 5
+    # RoPE tables are required only with rope = 1
+    assert L.vc_attn_prep(C.byref(shape()), C.byref(o), FAKE, FAKE, FAKE, None, None, None, None,
+                          C.byref(vc.Prepped(*([FAKE] * 8))), FAKE, 1 << 30, None) == 1
+
+
+def test_forward_and_group_validation(L):
+    o = vc.make_opts()
+    P = vc.Prepped(*([FAKE] * 8))
+    assert L.vc_attn_forward(C.byref(shape(Wd=15)), C.byref(o), C.byref(P), None, FAKE, None) == 2
+    assert L.vc_attn_forward(C.byref(shape()), C.byref(o), C.byref(P), None, None, None) == 1
+    assert L.vc_attn_forward(C.byref(shape()), C.byref(o), C.byref(P), FAKE + 2, FAKE, None) == 5
+    g = vc.make_group_opts(k=65)
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 3
+    g = vc.make_group_opts(iters=-1)
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 3
+    g = vc.make_group_opts()
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 16, None) == 4
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), None, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 1
+    g = vc.make_group_opts(mode=vc.GROUP_CUBE, cube=(0, 2, 16))
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, None, FAKE, FAKE, None, None, 0, None) == 3
+    g = vc.make_group_opts(mode=5)
+    assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, None, FAKE, FAKE, None, None, 0, None) == 3
+
+
+def test_workspace_size(L):
+    s = vc.make_shape(1, 12, (21, 39, 40))
+    o, g = vc.make_opts(), vc.make_group_opts()
+    a = vc.workspace_size(s, o, None)
+    b = vc.workspace_size(s, None, g)
+    assert a > 0 and b > 0 and vc.workspace_size(s, o, g) == max(a, b)
+    assert vc.workspace_size(shape(d=64), o, None) == 0
+
+
+def test_rope_tables_match_oracle(L):
+    for grid in [(4, 16, 16), (21, 39, 40), (21, 60, 60)]:
+        a = vc.rope_tables_host(*grid)
+        b = oracle.rope_tables(*grid)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_defaults(L):
+    o = vc.Opts(); L.vc_opts_default(C.byref(o))
+    assert (o.qk_fmt, o.p_mode, o.rope, o.hadamard, o.smooth_k, o.smooth_v) == (0, 0, 1, 1, 1, 1)
+    assert abs(o.beta + 0.35) < 1e-7 and o.sm_scale == 0.0
+    g = vc.GroupOpts(); L.vc_group_opts_default(C.byref(g))
+    assert (g.mode, g.k, g.iters, g.warm_start, tuple(g.cube)) == (2, 32, 8, 0, (4, 2, 16))
+
+
+def test_product_path_does_not_import_oracle():
+    import subprocess
+    import sys
+    code = ("import sys, paper_2609_15810_amd as vc; vc.lib(); "
+            "assert not any(m == 'oracle' or m.startswith('oracle.') for m in sys.modules), 'oracle imported'")
+    subprocess.run([sys.executable, "-c", code], check=True, cwd=ROOT)
+    for f in os.listdir(os.path.join(ROOT, "paper_2609_15810_amd")):
+        if f.endswith(".py"):
+            assert "oracle" not in open(os.path.join(ROOT, "paper_2609_15810_amd", f)).read(), f
