@@ -29,19 +29,29 @@ __global__ void grp_zero(uint32_t* p, int n) {
   if (i < n) p[i] = 0u;
 }
 
+// Each workgroup reduces 64 KB of the head (16 chunks of 16 bytes per thread) before one atomic.
 __global__ __launch_bounds__(256) void grp_amax(GroupArgs a) {
+  __shared__ float red[4];
   const int bh = blockIdx.y;
   const size_t words = (size_t)a.N * D / 8;  // 16-byte chunks of the head
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const u4* src = reinterpret_cast<const u4*>(a.V + (size_t)bh * a.N * D);
   float m = 0.f;
-  if (i < words) {
-    const u4 w = reinterpret_cast<const u4*>(a.V + (size_t)bh * a.N * D)[i];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[q])), fabsf(bf16_hi(w[q]))));
+  for (int u = 0; u < 16; ++u) {
+    const size_t i = ((size_t)blockIdx.x * 16 + u) * 256 + threadIdx.x;
+    if (i < words) {
+      const u4 w = src[i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[q])), fabsf(bf16_hi(w[q]))));
+    }
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(a.scale) + bh, __float_as_uint(m));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(reinterpret_cast<unsigned int*>(a.scale) + bh,
+              __float_as_uint(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
 }
 
 __device__ __forceinline__ float head_amax(const GroupArgs& a, int bh) { return a.scale[bh]; }
@@ -170,10 +180,17 @@ __device__ __forceinline__ int32_t div_rne(long long num, long long den) {
 __global__ __launch_bounds__(128) void grp_update(GroupArgs a) {
   const int k = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
   long long S = 0, cnt = 0;
-  for (int b = 0; b < a.nblk; ++b) {
-    const size_t p = ((size_t)bh * a.nblk + b) * a.k + k;
-    S += a.sums[p * D + c];
-    cnt += a.counts[p];
+  for (int b0 = 0; b0 < a.nblk; b0 += 16) {   // integer sums: any order; loads issued 16 ahead
+    int32_t sv[16], cv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const size_t p = ((size_t)bh * a.nblk + min(b0 + u, a.nblk - 1)) * a.k + k;
+      sv[u] = a.sums[p * D + c];
+      cv[u] = a.counts[p];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (b0 + u < a.nblk) { S += sv[u]; cnt += cv[u]; }
   }
   if (cnt > 0) a.cent[((size_t)bh * a.k + k) * D + c] = div_rne(S, cnt);
 }
@@ -266,7 +283,7 @@ hipError_t launch_group(const GroupArgs& a, int BH, hipStream_t s) {
   }
   grp_zero<<<(BH + 255) / 256, 256, 0, s>>>(reinterpret_cast<uint32_t*>(a.scale), BH);
   const size_t words = (size_t)a.N * D / 8;
-  grp_amax<<<dim3((unsigned)((words + 255) / 256), BH), 256, 0, s>>>(a);
+  grp_amax<<<dim3((unsigned)((words + 4095) / 4096), BH), 256, 0, s>>>(a);
   grp_codes<<<tok, 256, 0, s>>>(a);
   grp_init<<<dim3(a.k, BH), 128, 0, s>>>(a);
   const int rounds = a.iters > 0 ? a.iters : 1;

@@ -48,12 +48,12 @@ __global__ __launch_bounds__(128) void prep_stats(PrepArgs a) {
     if (!a.smooth_k) return;
     const uint32_t* K = reinterpret_cast<const uint32_t*>(a.K) + head * 64 + p;
     float s0 = 0.f, s1 = 0.f;
-    for (int r = 0; r < valid; r += 8) {
-      uint32_t w[8];
+    for (int r = 0; r < valid; r += 32) {
+      uint32_t w[32];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) w[u] = (r + u < valid) ? K[(size_t)(r0 + r + u) * 64] : 0u;
+      for (int u = 0; u < 32; ++u) w[u] = (r + u < valid) ? K[(size_t)(r0 + r + u) * 64] : 0u;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 32; ++u) {
         if (r + u < valid) {
           float x0 = bf16_lo(w[u]), x1 = bf16_hi(w[u]);
           if (a.rope) rope_pair(x0, x1, p, r0 + r + u, a);
@@ -69,16 +69,16 @@ __global__ __launch_bounds__(128) void prep_stats(PrepArgs a) {
     const uint32_t* V = reinterpret_cast<const uint32_t*>(a.V) + head * 64 + p;
     const int32_t* perm = a.perm ? a.perm + head : nullptr;
     float s0 = 0.f, s1 = 0.f;
-    for (int r = 0; r < valid; r += 8) {
-      uint32_t w[8];
+    for (int r = 0; r < valid; r += 32) {
+      uint32_t w[32];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 32; ++u) {
         const int row = r0 + r + u;
         const int n = perm ? clamp_index(perm[min(row, a.N - 1)], a.N) : row;
         w[u] = (r + u < valid) ? V[(size_t)n * 64] : 0u;
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 32; ++u) {
         if (r + u < valid) {
           vrows[r + u][p] = w[u];
           s0 = s0 + bf16_lo(w[u]);
@@ -120,13 +120,26 @@ __global__ __launch_bounds__(128) void prep_finalize(PrepArgs a) {
   if (a.smooth_k) {
     const float* part = a.ws_ksum + (size_t)bh * a.T * D + c;
     float tot = 0.f;
-    for (int j = 0; j < a.T; ++j) tot = tot + part[(size_t)j * D];
+    for (int j0 = 0; j0 < a.T; j0 += 16) {   // sequential sum over blocks; loads issued 16 ahead
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = part[(size_t)min(j0 + u, a.T - 1) * D];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (j0 + u < a.T) tot = tot + v[u];
+    }
     km = tot / (float)a.N;
   }
   a.k_mean[(size_t)bh * D + c] = km;
   const float* am = a.ws_vamax + (size_t)bh * a.T * D + c;
   float amax = 0.f;
-  for (int j = 0; j < a.T; ++j) amax = fmaxf(amax, am[(size_t)j * D]);
+  for (int j0 = 0; j0 < a.T; j0 += 16) {
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = am[(size_t)min(j0 + u, a.T - 1) * D];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) amax = fmaxf(amax, v[u]);
+  }
   a.v_scale[(size_t)bh * D + c] = amax > 0.f ? amax / 448.f : 1.f;
   a.ws_vinv[(size_t)bh * D + c] = amax > 0.f ? 448.f / amax : 0.f;
 }
