@@ -1,0 +1,158 @@
+"""GPU parity at the full workload sizes, in the launch configuration the benchmark times.
+
+* 32760-token layer (B=1, H=12, 21x39x40 grid): k-means grouping, preprocessing codes on all heads
+  bit-exact; attention on sampled query rows (first, middle and the ragged last query block of
+  every head) within the tolerance.
+* 75600-token layer (B=1, H=40, 21x60x60 grid): the same on all heads for grouping and codes,
+  attention on sampled rows of a few heads; then a drifted call (inputs + 0.05 N(0,1)) reusing the
+  permutation of the first call.
+* Denoising-loop slice: inputs interpolated between two seeded fields; grouping at call 0 (cold)
+  and call 4 (warm-started from call 0's centroids), bit-exact.
+"""
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synthetic as S
+from test_gpu_parity import assert_prep_equal, check_output, dev16, dev32, f32_bits
+from layouts import untile_qk, untile_v
+
+torch = pytest.importorskip("torch")
+vc = pytest.importorskip("paper_2609_15810_amd")
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def log(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def run_gpu(name, Q, K, V, A=None, regroup=True):
+    w = S.WORKLOADS[name]
+    if A is None:
+        A = vc.Attention(w.B, w.H, w.grid)
+    Qd, Kd, Vd = dev16(Q), dev16(K), dev16(V)
+    if regroup:
+        A.group(Vd)
+    A.prep(Qd, Kd, Vd)
+    O = torch.empty((w.B, w.H, w.N, 128), dtype=torch.int16, device="cuda")
+    A.forward(O)
+    torch.cuda.synchronize()
+    return A, S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(w.B * w.H, w.N, 128).astype(np.float64)
+
+
+def host_prepped(A):
+    pp = A.prepped
+    return dict(q=untile_qk(pp.q.cpu().numpy()), q_scale=pp.q_scale.cpu().numpy(), k=untile_qk(pp.k.cpu().numpy()),
+                k_scale=pp.k_scale.cpu().numpy(), k_mean=pp.k_mean.cpu().numpy(), v=untile_v(pp.v.cpu().numpy()),
+                v_scale=pp.v_scale.cpu().numpy(), v_mean=pp.v_mean.cpu().numpy().view(np.uint16))
+
+
+def sample_rows(N):
+    T = (N + 127) // 128
+    blocks = [0, T // 2, T - 1]
+    return np.concatenate([np.arange(128 * b, min(N, 128 * b + 128)) for b in blocks]).astype(np.int32)
+
+
+@pytest.mark.timeout(900)
+def test_dit_small_full():
+    name = "dit_small"
+    w = S.WORKLOADS[name]
+    log("generating inputs")
+    Q, K, V = S.make_qkv(name, seed=0)
+    log("GPU group + prep + forward")
+    A, o = run_gpu(name, Q, K, V)
+    log("oracle grouping")
+    g = oracle.group(V, w.grid, k=32, iters=8)
+    for key in ("labels", "perm", "inv_perm"):
+        assert np.array_equal(getattr(A, key).cpu().numpy(), g[key]), key
+    assert np.array_equal(f32_bits(A.centroids.cpu().numpy()), f32_bits(g["centroids"]))
+    log("oracle preprocessing")
+    pp = oracle.prep(Q, K, V, w.grid, perm=g["perm"])
+    assert_prep_equal(host_prepped(A), pp, name)
+    rows = sample_rows(w.N)
+    log(f"oracle attention on {rows.size} rows x {w.H} heads")
+    ref = oracle.attention(pp, rows)
+    check_output(o[:, rows], ref, name)
+
+
+@pytest.mark.timeout(1200)
+def test_dit_large_full_and_drift():
+    name = "dit_large"
+    w = S.WORKLOADS[name]
+    log("generating inputs")
+    Q, K, V = S.make_qkv(name, seed=0)
+    log("GPU group + prep + forward")
+    A, o = run_gpu(name, Q, K, V)
+    log("oracle grouping (40 heads)")
+    g = oracle.group(V, w.grid, k=32, iters=8)
+    assert np.array_equal(A.perm.cpu().numpy(), g["perm"])
+    assert np.array_equal(A.labels.cpu().numpy(), g["labels"])
+    assert np.array_equal(f32_bits(A.centroids.cpu().numpy()), f32_bits(g["centroids"]))
+    log("oracle preprocessing (40 heads)")
+    pp = oracle.prep(Q, K, V, w.grid, perm=g["perm"])
+    assert_prep_equal(host_prepped(A), pp, name)
+    del pp
+    rows = sample_rows(w.N)
+    heads = [0, 17, 39]
+    log(f"oracle attention on {rows.size} rows x {len(heads)} heads")
+    pph = oracle.prep(Q[:, heads], K[:, heads], V[:, heads], w.grid, perm=g["perm"][:, heads])
+    ref = oracle.attention(pph, rows)
+    check_output(o[heads][:, rows], ref, name)
+    # drifted call: inputs + 0.05 N(0,1), permutation of the first call reused
+    log("drifted call 3 reusing the permutation")
+    Q3, K3, V3 = S.make_qkv(name, seed=0, call=3, drift=0.05, heads=heads)
+    Qs, Ks, Vs = (np.ascontiguousarray(x[:, heads]) for x in (Q3, K3, V3))
+    sub = vc.Attention(1, len(heads), w.grid)
+    sub.perm.copy_(torch.from_numpy(np.ascontiguousarray(g["perm"][:, heads])).cuda())
+    _, o3 = run_gpu_sub(sub, Qs, Ks, Vs, w)
+    pp3 = oracle.prep(Qs, Ks, Vs, w.grid, perm=g["perm"][:, heads])
+    assert_prep_equal(host_prepped(sub), pp3, name + " drift")
+    check_output(o3[:, rows], oracle.attention(pp3, rows), name + " drift")
+
+
+def run_gpu_sub(A, Q, K, V, w):
+    A.prep(dev16(Q), dev16(K), dev16(V))
+    O = torch.empty((1, Q.shape[1], w.N, 128), dtype=torch.int16, device="cuda")
+    A.forward(O)
+    torch.cuda.synchronize()
+    return A, S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(Q.shape[1], w.N, 128).astype(np.float64)
+
+
+@pytest.mark.timeout(900)
+def test_loop_slice_warm_regroup():
+    name = "dit_small"
+    w = S.WORKLOADS[name]
+    heads = [0, 5, 11]
+    log("call 0 (cold grouping)")
+    Q0, K0, V0 = (np.ascontiguousarray(x[:, heads]) for x in S.make_interpolated(name, 0, heads=heads))
+    A = vc.Attention(1, len(heads), w.grid)
+    A.group(dev16(V0))
+    torch.cuda.synchronize()
+    g0 = oracle.group(V0, w.grid, k=32, iters=8)
+    assert np.array_equal(A.perm.cpu().numpy(), g0["perm"])
+    log("call 4 (warm grouping from call 0's centroids, 4 rounds)")
+    Q4, K4, V4 = (np.ascontiguousarray(x[:, heads]) for x in S.make_interpolated(name, 4, heads=heads))
+    A.gopts = vc.make_group_opts(k=32, iters=4, warm_start=True)
+    A.group(dev16(V4))
+    torch.cuda.synchronize()
+    g4 = oracle.group(V4, w.grid, k=32, iters=4, warm_start=True, cent_in=g0["centroids"])
+    assert np.array_equal(A.perm.cpu().numpy(), g4["perm"])
+    assert np.array_equal(f32_bits(A.centroids.cpu().numpy()), f32_bits(g4["centroids"]))
+    A.prep(dev16(Q4), dev16(K4), dev16(V4))
+    O = torch.empty((1, len(heads), w.N, 128), dtype=torch.int16, device="cuda")
+    A.forward(O)
+    torch.cuda.synchronize()
+    o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(len(heads), w.N, 128).astype(np.float64)
+    pp = oracle.prep(Q4, K4, V4, w.grid, perm=g4["perm"])
+    assert_prep_equal(host_prepped(A), pp, "loop call 4")
+    rows = sample_rows(w.N)
+    check_output(o[:, rows], oracle.attention(pp, rows), "loop call 4")
