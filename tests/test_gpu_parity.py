@@ -173,6 +173,21 @@ def test_forward_ragged_perm(flags):
     check_output(o.reshape(2, 1000, 128), ref, str(flags))
 
 
+@pytest.mark.parametrize("N", [1, 100, 200, 300, 500, 600, 700, 833, 1100, 1280, 1400, 2100])
+def test_forward_tile_counts(N):
+    """Every key-tile count from 1 to 11 and 17 (so every remainder of the tile loop, mean batches
+    of 8 that end full or partial) with a ragged last tile where N is not a multiple of 128."""
+    grid = (1, 1, N)
+    rng = np.random.default_rng(100 + N)
+    Q = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * 2).astype(np.float32))
+    K = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * 2 + rng.standard_normal(128) * 3).astype(np.float32))
+    V = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) + rng.standard_normal(128) * 2).astype(np.float32))
+    A, _ = gpu_prep(Q, K, V, grid)
+    o = gpu_forward(A)
+    ref = oracle.attention(oracle.prep(Q, K, V, grid), np.arange(N))
+    check_output(o.reshape(2, N, 128), ref, f"N={N}")
+
+
 def test_forward_deterministic():
     Q, K, V = S.make_qkv("tiny")
     grid = S.WORKLOADS["tiny"].grid
