@@ -3,12 +3,16 @@
 //
 // KMEANS: Lloyd rounds on per-head INT8 codes of V (scale amax/127 over the head).
 //   grp_amax     per-head max |V| (exact, order-free: integer max of non-negative float bits)
-//   grp_codes    INT8 codes, row-major [N][128]
+//   grp_codes    INT8 codes, row-major [N][128], plus a token-interleaved copy for the member
+//                sums (per 32-token block, per 32-channel block and lane half: 16 consecutive
+//                tokens of one channel; transposed through LDS)
 //   grp_init     initial integer centroids (tokens floor((2c+1)N/(2k)), or the caller's fp32
 //                centroids requantized)
-//   grp_assign   256 tokens per workgroup: squared-L2 argmin |C|^2 - 2 x.C in int32 with
-//                v_dot4 (ties to the smallest cluster), then exact integer member sums and
-//                counts of the workgroup's tokens (partials, reduced by grp_update)
+//   grp_assign   1024 tokens per workgroup, 32 per wave step, on the matrix cores: the INT8
+//                product C X^T gives |C|^2 - 2 x.C exactly in int32, the argmin is one integer
+//                min over (distance << 7 | cluster) (ties to the smallest cluster); then the
+//                exact member sums O X with the one-hot label matrix O as the INT8 A operand,
+//                and the counts (partials per workgroup, reduced by grp_update)
 //   grp_update   centroid = round-half-even integer mean of the members (exact int64 division)
 // Integer arithmetic throughout makes labels, centroids and the permutation reproducible bit for
 // bit regardless of the order in which partial sums are combined.
@@ -56,38 +60,95 @@ __global__ __launch_bounds__(256) void grp_amax(GroupArgs a) {
 
 __device__ __forceinline__ float head_amax(const GroupArgs& a, int bh) { return a.scale[bh]; }
 
+// 256 tokens per workgroup: each thread quantizes one token into its row-major row and into LDS;
+// then 4x4 byte transposes through LDS write the token-interleaved copy with 16-byte stores.
 __global__ __launch_bounds__(256) void grp_codes(GroupArgs a) {
-  const int bh = blockIdx.y;
-  const int n = blockIdx.x * 256 + threadIdx.x;
-  if (n >= a.N) return;
+  __shared__ __attribute__((aligned(16))) uint32_t xs[256][D / 4 + 1];
+  const int bh = blockIdx.y, t = threadIdx.x;
+  const int n = blockIdx.x * 256 + t;
   const float amax = head_amax(a, bh);
   const float inv = amax > 0.f ? 127.f / amax : 0.f;
-  const u4* src = reinterpret_cast<const u4*>(a.V + ((size_t)bh * a.N + n) * D);
-  u4* dst = reinterpret_cast<u4*>(a.codes + ((size_t)bh * a.N + n) * D);
+  if (n < a.N) {
+    const u4* src = reinterpret_cast<const u4*>(a.V + ((size_t)bh * a.N + n) * D);
+    u4* dst = reinterpret_cast<u4*>(a.codes + ((size_t)bh * a.N + n) * D);
 #pragma unroll
-  for (int ch = 0; ch < 8; ++ch) {   // 16 channels per chunk
-    const u4 w0 = src[2 * ch], w1 = src[2 * ch + 1];
-    uint32_t out[4];
+    for (int ch = 0; ch < 8; ++ch) {   // 16 channels per chunk
+      const u4 w0 = src[2 * ch], w1 = src[2 * ch + 1];
+      uint32_t out[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t w = q < 2 ? w0[2 * q] : w1[2 * (q - 2)];
-      const uint32_t v = q < 2 ? w0[2 * q + 1] : w1[2 * (q - 2) + 1];
-      float f[4] = {bf16_lo(w), bf16_hi(w), bf16_lo(v), bf16_hi(v)};
-      uint32_t pk = 0;
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t w = q < 2 ? w0[2 * q] : w1[2 * (q - 2)];
+        const uint32_t v = q < 2 ? w0[2 * q + 1] : w1[2 * (q - 2) + 1];
+        float f[4] = {bf16_lo(w), bf16_hi(w), bf16_lo(v), bf16_hi(v)};
+        uint32_t pk = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float r = __builtin_rintf(f[e] * inv);
-        r = fminf(fmaxf(r, -127.f), 127.f);
-        pk |= ((uint32_t)((int)r & 0xff)) << (8 * e);
+        for (int e = 0; e < 4; ++e) {
+          float r = __builtin_rintf(f[e] * inv);
+          r = fminf(fmaxf(r, -127.f), 127.f);
+          pk |= ((uint32_t)((int)r & 0xff)) << (8 * e);
+        }
+        out[q] = pk;
+        xs[t][4 * ch + q] = pk;
       }
-      out[q] = pk;
+      dst[ch] = u4{out[0], out[1], out[2], out[3]};
     }
-    dst[ch] = u4{out[0], out[1], out[2], out[3]};
+  } else {
+#pragma unroll
+    for (int w = 0; w < D / 4; ++w) xs[t][w] = 0u;   // padded tokens: zero codes
+  }
+  __syncthreads();
+  // unit (block b of 32 tokens, lane half kh, channels 4g..4g+3): 16 tokens x 4 channels
+  const int ntb = (a.N + 31) / 32;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int unit = u * 256 + t;
+    const int g = unit & 31, kh = (unit >> 5) & 1, b = unit >> 6;
+    const int tb = blockIdx.x * 8 + b;
+    if (tb >= ntb) continue;
+    uint32_t col[4][4];   // col[j][tq]: channel 4g+j of tokens 4tq..4tq+3 (of the 16)
+#pragma unroll
+    for (int tq = 0; tq < 4; ++tq) {
+      uint32_t r[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) r[e] = xs[b * 32 + kh * 16 + 4 * tq + e][g];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        col[j][tq] = ((r[0] >> (8 * j)) & 0xffu) | (((r[1] >> (8 * j)) & 0xffu) << 8) |
+                     (((r[2] >> (8 * j)) & 0xffu) << 16) | (((r[3] >> (8 * j)) & 0xffu) << 24);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = 4 * g + j, db = c >> 5, cl = c & 31;
+      u4* dst = reinterpret_cast<u4*>(a.codesT + ((size_t)bh * ntb + tb) * (32 * D) + (((db * 2 + kh) * 32 + cl) * 16));
+      *dst = u4{col[j][0], col[j][1], col[j][2], col[j][3]};
+    }
   }
 }
 
-__global__ __launch_bounds__(128) void grp_init(GroupArgs a) {
+constexpr int NORM_PAD = 8388000;    // |C|^2 of a padding cluster: above every real distance
+
+// Centroid k of head bh is kept three ways: int32 (the exact state of the Lloyd rounds), int8
+// (the assignment's A operand; the values are means of int8 codes, so they fit) and its squared
+// norm. Rows k..KMAX-1 are padding: zero codes, norm NORM_PAD. One thread per channel.
+__device__ __forceinline__ void publish_centroid(const GroupArgs& a, int bh, int k, int c, int32_t v) {
+  __shared__ int32_t red[D / 64];
+  a.cent[((size_t)bh * a.k + k) * D + c] = v;
+  a.cent8[((size_t)bh * KMAX + k) * D + c] = (int8_t)v;
+  int32_t sq = v * v;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+  if ((c & 63) == 0) red[c >> 6] = sq;
+  __syncthreads();
+  if (c == 0) a.cnorm[(size_t)bh * KMAX + k] = red[0] + red[1];
+}
+
+__global__ __launch_bounds__(D) void grp_init(GroupArgs a) {
   const int k = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  if (k >= a.k) {   // padding rows
+    a.cent8[((size_t)bh * KMAX + k) * D + c] = 0;
+    if (c == 0) a.cnorm[(size_t)bh * KMAX + k] = NORM_PAD;
+    return;
+  }
   int32_t v;
   if (a.warm_start) {
     const float amax = head_amax(a, bh);
@@ -99,75 +160,150 @@ __global__ __launch_bounds__(128) void grp_init(GroupArgs a) {
     const long long n0 = ((long long)(2 * k + 1) * a.N) / (2LL * a.k);
     v = a.codes[((size_t)bh * a.N + n0) * D + c];
   }
-  a.cent[((size_t)bh * a.k + k) * D + c] = v;
+  publish_centroid(a, bh, k, c, v);
 }
 
-__global__ __launch_bounds__(GT) void grp_assign(GroupArgs a) {
-  __shared__ int32_t cent8[KMAX][D / 4];   // centroids as packed int8 words
-  __shared__ int32_t norm[KMAX];
-  __shared__ uint8_t xs[GT][D + 4];
-  __shared__ int32_t lab[GT];
-  __shared__ int32_t acc[2][KMAX][D];
-  const int blk = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
-  const int K = a.k;
-  const int32_t* C = a.cent + (size_t)bh * K * D;
-  for (int idx = t; idx < K * (D / 4); idx += GT) {
-    const int k = idx / (D / 4), w = idx % (D / 4);
-    const int32_t* c4 = C + (size_t)k * D + 4 * w;
-    cent8[k][w] = (c4[0] & 0xff) | ((c4[1] & 0xff) << 8) | ((c4[2] & 0xff) << 16) | ((c4[3] & 0xff) << 24);
-  }
-  for (int idx = t; idx < 2 * KMAX * D; idx += GT) (&acc[0][0][0])[idx] = 0;
-  if (t < K) {
-    int32_t s = 0;
-    for (int c = 0; c < D; ++c) s += C[(size_t)t * D + c] * C[(size_t)t * D + c];
-    norm[t] = s;
-  }
-  __syncthreads();
+constexpr int AW = 4;            // waves per assignment workgroup
+constexpr int AG = 8;            // 32-token steps per wave
+constexpr int ATOK = AW * AG * 32;   // 1024 tokens per assignment workgroup
 
-  const int n = blk * GT + t;
-  const bool valid = n < a.N;
-  int32_t xw[D / 4];
-  const u4* src = reinterpret_cast<const u4*>(a.codes + ((size_t)bh * a.N + (valid ? n : 0)) * D);
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const u4 w = src[q];
-    xw[4 * q] = (int32_t)w[0]; xw[4 * q + 1] = (int32_t)w[1]; xw[4 * q + 2] = (int32_t)w[2]; xw[4 * q + 3] = (int32_t)w[3];
+// One Lloyd assignment on the matrix cores (KB = clusters / 32, rounded up). Per 32-token step:
+//   S^T = C X^T     INT8 MFMA 32x32x32, A = centroid rows (registers), B = the tokens' codes;
+//                   lane (token l%32, half l/32) holds 16 clusters' x.C, the other 16 in lane l^32
+//   key  = (|C|^2 - 2 x.C + 2^23) << 7 | cluster, argmin = integer min of the keys (the distance
+//          fits 24 bits, the cluster 7 bits; equal distances resolve to the smaller cluster)
+//   sums += O X     INT8 MFMA, A = one-hot labels (cluster rows x 32 tokens), B = the
+//                   token-interleaved codes (16 consecutive tokens of one channel per lane)
+//   counts         popcounts of the one-hot bytes
+// The wave's sums stay in registers; at the end they are added into LDS and written as one
+// partial per workgroup.
+template <int KB>
+__global__ __launch_bounds__(AW * 64) void grp_assign(GroupArgs a) {
+  __shared__ int32_t acc[KB * 32][D];
+  __shared__ int32_t cntl[KB * 32];
+  __shared__ int32_t norm[KB * 32];
+  __shared__ __attribute__((aligned(16))) uint8_t lab[AW][32];
+  const int bh = blockIdx.y, wg = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kh = lane >> 5, col = lane & 31, K = a.k, N = a.N;
+  for (int i = tid; i < KB * 32 * D; i += AW * 64) (&acc[0][0])[i] = 0;
+  if (tid < KB * 32) {
+    norm[tid] = a.cnorm[(size_t)bh * KMAX + tid];
+    cntl[tid] = 0;
   }
-  int best = 0;
-  int32_t bd = 0;
-  for (int k = 0; k < K; ++k) {
-    int32_t dot = 0;
+  // centroid rows as the A operand (padding clusters are zero rows) and the lane's norms
+  v4i ca[KB][4];
+  int32_t nr[KB][16];
 #pragma unroll
-    for (int w = 0; w < D / 4; ++w) dot = __builtin_amdgcn_sdot4(xw[w], cent8[k][w], dot, false);
-    const int32_t dist = norm[k] - 2 * dot;
-    if (k == 0 || dist < bd) { bd = dist; best = k; }
-  }
-  lab[t] = valid ? best : -1;
-  if (valid) a.labels[(size_t)bh * a.N + n] = best;
+  for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
-  for (int w = 0; w < D / 4; ++w) *reinterpret_cast<int32_t*>(&xs[t][4 * w]) = xw[w];
+    for (int dc = 0; dc < 4; ++dc)
+      ca[cb][dc] = *reinterpret_cast<const v4i*>(a.cent8 + ((size_t)bh * KMAX + 32 * cb + col) * D + 32 * dc + 16 * kh);
   __syncthreads();
+#pragma unroll
+  for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) nr[cb][r] = norm[32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3)];
 
-  // exact member sums of this block: thread (half, c) walks its 128 tokens
-  {
-    const int c = t & (D - 1), half = t >> 7;
-    for (int i = 0; i < GT / 2; ++i) {
-      const int tok = half * (GT / 2) + i;
-      const int L = lab[tok];
-      if (L >= 0) acc[half][L][c] += (int32_t)(int8_t)xs[tok][c];
+  const int ntb = (N + 31) / 32;
+  const int8_t* codes = a.codes + (size_t)bh * N * D;
+  const int8_t* codesT = a.codesT + (size_t)bh * ntb * (32 * D);
+  v16i sums[KB][4];
+#pragma unroll
+  for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sums[cb][db][r] = 0;
+  int32_t cntp[KB];
+#pragma unroll
+  for (int cb = 0; cb < KB; ++cb) cntp[cb] = 0;
+
+  auto load_step = [&](int n0, v4i (&xb)[4], v4i (&xt)[4]) {
+    const int token = min(n0 + col, N - 1);
+    const int8_t* xr = codes + (size_t)token * D + 16 * kh;
+#pragma unroll
+    for (int dc = 0; dc < 4; ++dc) xb[dc] = *reinterpret_cast<const v4i*>(xr + 32 * dc);
+    const int8_t* xc = codesT + (size_t)(n0 >> 5) * (32 * D) + (kh * 32 + col) * 16;
+#pragma unroll
+    for (int db = 0; db < 4; ++db) xt[db] = *reinterpret_cast<const v4i*>(xc + db * 1024);
+  };
+  const int nbase = wg * ATOK + wave * (AG * 32);
+  v4i xb[4], xt[4];
+  if (nbase < N) load_step(nbase, xb, xt);
+  for (int g = 0; g < AG; ++g) {
+    const int n0 = nbase + g * 32;
+    if (n0 >= N) break;
+    v4i xbn[4], xtn[4];
+    if (g + 1 < AG && n0 + 32 < N) load_step(n0 + 32, xbn, xtn);   // next step's codes in flight
+    int best = 0x7fffffff;
+#pragma unroll
+    for (int cb = 0; cb < KB; ++cb) {
+      v16i S = {};
+#pragma unroll
+      for (int dc = 0; dc < 4; ++dc) S = __builtin_amdgcn_mfma_i32_32x32x32_i8(ca[cb][dc], xb[dc], S, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = ((nr[cb][r] - 2 * S[r] + (1 << 23)) << 7) | (32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3));
+        best = min(best, key);
+      }
+    }
+    best = min(best, __shfl_xor(best, 32));
+    const int token = n0 + col;
+    const bool valid = token < N;
+    const int label = valid ? (best & 127) : 255;
+    if (valid && kh == 0) a.labels[(size_t)bh * N + token] = label;
+    if (kh == 0) lab[wave][col] = (uint8_t)label;
+    // the wave's 32 labels: one-hot bytes of (cluster row, token) for this lane's 16 tokens
+    const u4 l4 = *reinterpret_cast<const u4*>(&lab[wave][16 * kh]);
+#pragma unroll
+    for (int cb = 0; cb < KB; ++cb) {
+      const uint32_t rep = (uint32_t)(32 * cb + col) * 0x01010101u;
+      int32_t oh[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t x = l4[q] ^ rep;
+        const uint32_t nz = (((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x) & 0x80808080u;   // 0x80 where byte != 0
+        oh[q] = (int32_t)((~nz >> 7) & 0x01010101u);
+        cntp[cb] += __builtin_popcount((uint32_t)oh[q]);
+      }
+      const v4i ohv = {oh[0], oh[1], oh[2], oh[3]};
+#pragma unroll
+      for (int db = 0; db < 4; ++db) sums[cb][db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ohv, xt[db], sums[cb][db], 0, 0, 0);
+    }
+    if (g + 1 < AG && n0 + 32 < N) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { xb[q] = xbn[q]; xt[q] = xtn[q]; }
     }
   }
+  // this wave's sums and counts into the workgroup's LDS accumulators
+#pragma unroll
+  for (int cb = 0; cb < KB; ++cb) {
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3);
+        if (row < K) atomicAdd(&acc[row][32 * db + col], sums[cb][db][r]);
+      }
+    if (32 * cb + col < K) atomicAdd(&cntl[32 * cb + col], cntp[cb]);
+  }
   __syncthreads();
-  const size_t pbase = ((size_t)bh * a.nblk + blk) * K;
-  for (int idx = t; idx < K * D; idx += GT) {
-    const int k = idx / D, c = idx % D;
-    a.sums[(pbase + k) * D + c] = acc[0][k][c] + acc[1][k][c];
-  }
-  if (t < K) {
-    int32_t cnt = 0;
-    for (int i = 0; i < GT; ++i) cnt += (lab[i] == t);
-    a.counts[pbase + t] = cnt;
-  }
+  const size_t part = (size_t)bh * a.npart + wg;
+  for (int i = tid; i < K * D; i += AW * 64) a.sums[part * K * D + i] = (&acc[0][0])[i];
+  if (tid < K) a.counts[part * K + tid] = cntl[tid];
+}
+
+// per-256-token-block label counts of the final labels (the stable sort's histogram)
+__global__ __launch_bounds__(GT) void grp_hist(GroupArgs a) {
+  __shared__ int32_t h[KMAX];
+  const int blk = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+  if (t < KMAX) h[t] = 0;
+  __syncthreads();
+  const int n = blk * GT + t;
+  if (n < a.N) atomicAdd(&h[a.labels[(size_t)bh * a.N + n]], 1);
+  __syncthreads();
+  if (t < a.nlab) a.counts[((size_t)bh * a.nblk + blk) * a.nlab + t] = h[t];
 }
 
 __device__ __forceinline__ int32_t div_rne(long long num, long long den) {
@@ -177,22 +313,22 @@ __device__ __forceinline__ int32_t div_rne(long long num, long long den) {
   return (int32_t)q;
 }
 
-__global__ __launch_bounds__(128) void grp_update(GroupArgs a) {
+__global__ __launch_bounds__(D) void grp_update(GroupArgs a) {
   const int k = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
   long long S = 0, cnt = 0;
-  for (int b0 = 0; b0 < a.nblk; b0 += 16) {   // integer sums: any order; loads issued 16 ahead
-    int32_t sv[16], cv[16];
+  for (int b0 = 0; b0 < a.npart; b0 += 32) {   // integer sums: any order; loads issued 32 ahead
+    int32_t sv[32], cv[32];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const size_t p = ((size_t)bh * a.nblk + min(b0 + u, a.nblk - 1)) * a.k + k;
+    for (int u = 0; u < 32; ++u) {
+      const size_t p = ((size_t)bh * a.npart + min(b0 + u, a.npart - 1)) * a.k + k;
       sv[u] = a.sums[p * D + c];
       cv[u] = a.counts[p];
     }
 #pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (b0 + u < a.nblk) { S += sv[u]; cnt += cv[u]; }
+    for (int u = 0; u < 32; ++u)
+      if (b0 + u < a.npart) { S += sv[u]; cnt += cv[u]; }
   }
-  if (cnt > 0) a.cent[((size_t)bh * a.k + k) * D + c] = div_rne(S, cnt);
+  if (cnt > 0) publish_centroid(a, bh, k, c, div_rne(S, cnt));   // an empty cluster keeps its centroid
 }
 
 __global__ __launch_bounds__(128) void grp_cent_out(GroupArgs a) {
@@ -285,13 +421,15 @@ hipError_t launch_group(const GroupArgs& a, int BH, hipStream_t s) {
   const size_t words = (size_t)a.N * D / 8;
   grp_amax<<<dim3((unsigned)((words + 4095) / 4096), BH), 256, 0, s>>>(a);
   grp_codes<<<tok, 256, 0, s>>>(a);
-  grp_init<<<dim3(a.k, BH), 128, 0, s>>>(a);
+  grp_init<<<dim3(KMAX, BH), D, 0, s>>>(a);
   const int rounds = a.iters > 0 ? a.iters : 1;
   for (int it = 0; it < rounds; ++it) {
-    grp_assign<<<dim3(a.nblk, BH), GT, 0, s>>>(a);
+    if (a.k <= 32) grp_assign<1><<<dim3(a.npart, BH), AW * 64, 0, s>>>(a);
+    else grp_assign<2><<<dim3(a.npart, BH), AW * 64, 0, s>>>(a);
     if (a.iters > 0) grp_update<<<dim3(a.k, BH), 128, 0, s>>>(a);
   }
   grp_cent_out<<<dim3(a.k, BH), 128, 0, s>>>(a);
+  grp_hist<<<dim3(a.nblk, BH), GT, 0, s>>>(a);
   grp_offsets<<<BH, 256, 0, s>>>(a);
   grp_scatter<<<dim3(a.nblk, BH), GT, 0, s>>>(a);
   return hipGetLastError();

@@ -45,12 +45,16 @@ struct GroupArgs {
   float* centroids;
   int32_t *labels, *perm, *inv_perm;
   int8_t* codes;     // workspace: per-head INT8 codes of V [B*H][N][128]
+  int8_t* codesT;    // workspace: the same codes token-interleaved [B*H][ceil(N/32)][4][2][32][16]
   float* scale;      // workspace: [B*H] amax (then scale)
   int32_t* cent;     // workspace: [B*H][k][128] integer centroids
-  int32_t* sums;     // workspace: [B*H][k][128] member sums
-  int32_t* counts;   // workspace: [B*H][k]
+  int8_t* cent8;     // workspace: [B*H][64][128] the same as int8, rows k.. zero
+  int32_t* cnorm;    // workspace: [B*H][64] their squared norms, rows k.. a padding value
+  int32_t* sums;     // workspace: [B*H][npart][k][128] member sums per assignment workgroup
+  int32_t* counts;   // workspace: [B*H][npart][k] member counts, later [B*H][nblk][k] label histograms
   int32_t* blockhist;// workspace: [B*H][nblk][nlab] per-block label counts, then offsets
   int N, F, Ht, Wd, k, iters, warm_start, mode, cube_t, cube_h, cube_w, nlab, nblk;
+  int npart;         // assignment workgroups per head (1024 tokens each)
 };
 
 hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s);
