@@ -241,6 +241,8 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   a.F = shape->F;
   a.Ht = shape->Ht;
   a.Wd = shape->Wd;
+  a.inv_w = 1.0f / (float)shape->Wd;
+  a.inv_hw = 1.0f / (float)(shape->Ht * shape->Wd);
   a.rope = opts->rope;
   a.hadamard = opts->hadamard;
   a.smooth_k = opts->smooth_k;

@@ -1,10 +1,11 @@
 // Fused preprocessing of the 8-bit VC-Attention operands (Sec. 3.4 and Appendix B).
 //
-// Three launches per call:
-//   prep_stats    grid (T, B*H), 128 threads. Wave 0: rotated key rows of original-order block
-//                 j summed per channel (the centering statistics). Wave 1: value rows of
-//                 permuted block j (gathered by perm): the block mean mu_j, stored as bf16, and
-//                 the per-channel max |V' - mu_j| of the block.
+// Four launches per call:
+//   prep_kstats   grid (T, B*H), one wave: rotated key rows of original-order block j summed per
+//                 channel (the centering statistics).
+//   prep_vstats   grid (T, B*H), one wave: value rows of permuted block j (gathered by perm):
+//                 the block mean mu_j, stored as bf16, and the per-channel max |V' - mu_j| of
+//                 the block.
 //   prep_finalize grid (B*H), 128 threads: key channel mean and per-channel value scale.
 //   prep_quant    grid (T, B*H, 3), 256 threads. z = 0: Q rows (RoPE, Hadamard, per-block
 //                 INT8); z = 1: K' rows (gather, RoPE, centering, Hadamard, per-block INT8);
@@ -13,16 +14,45 @@
 // All floating-point steps that decide a stored code are written as single IEEE fp32
 // operations in a fixed order (compiled with -ffp-contract=off; fused multiply-adds are spelled
 // out), so the codes, scales and means are reproducible bit for bit.
+#include <type_traits>
+
 #include "vc_common.hpp"
 #include "vc_internal.hpp"
 
 namespace vc {
 
-// One rotary pair at token n: y0 = fma(x0, c, -(x1 s)), y1 = fma(x0, s, x1 c).
-__device__ __forceinline__ void rope_pair(float& x0, float& x1, int pair, int n, const PrepArgs& a) {
-  const int x = n % a.Wd, y = (n / a.Wd) % a.Ht, f = n / (a.Wd * a.Ht);
+// n / d for 0 <= n < 2^24 and d >= 1: a float estimate, then one correction each way (the
+// estimate is within one of the quotient).
+__device__ __forceinline__ int div_small(int n, int d, float inv_d) {
+  int q = (int)((float)n * inv_d);
+  q -= (q * d > n) ? 1 : 0;
+  q += ((q + 1) * d <= n) ? 1 : 0;
+  return q;
+}
+
+// Rows of the rotary tables for token n: frames axis f, rows axis F + y, columns axis F + Ht + x
+// (token n = (f * Ht + y) * Wd + x).
+struct RopeRows {
+  int f, y, x;
+};
+__device__ __forceinline__ RopeRows rope_rows(int n, const PrepArgs& a) {
+  int f, rem, y;
+  if (a.N <= (1 << 24)) {
+    f = div_small(n, a.Ht * a.Wd, a.inv_hw);
+    rem = n - f * (a.Ht * a.Wd);
+    y = div_small(rem, a.Wd, a.inv_w);
+  } else {
+    f = n / (a.Ht * a.Wd);
+    rem = n - f * (a.Ht * a.Wd);
+    y = rem / a.Wd;
+  }
+  return RopeRows{f, a.F + y, a.F + a.Ht + (rem - y * a.Wd)};
+}
+
+// One rotary pair with the table row of its axis: y0 = fma(x0, c, -(x1 s)), y1 = fma(x0, s, x1 c).
+__device__ __forceinline__ void rope_pair(float& x0, float& x1, int pair, const RopeRows& rr, const PrepArgs& a) {
   const int ax = rope_axis(pair);
-  const int row = ax == 0 ? f : (ax == 1 ? a.F + y : a.F + a.Ht + x);
+  const int row = ax == 0 ? rr.f : (ax == 1 ? rr.y : rr.x);
   const float c = a.rope_cos[row * 64 + pair], s = a.rope_sin[row * 64 + pair];
   const float p = x1 * s, q = x1 * c;
   const float y0 = __builtin_fmaf(x0, c, -p);
@@ -36,55 +66,81 @@ __device__ __forceinline__ void rope_pair(float& x0, float& x1, int pair, int n,
 // Lane p of a wave owns channels (2p, 2p+1) and walks the block's rows in ascending order, so
 // every per-channel sum is a sequential fp32 sum from 0.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(128) void prep_stats(PrepArgs a) {
-  __shared__ uint32_t vrows[BLK][64];  // the block's gathered value rows, for the second pass
-  const int j = blockIdx.x, bh = blockIdx.y;
-  const int wave = threadIdx.x >> 6, p = threadIdx.x & 63;
+__global__ __launch_bounds__(64) void prep_kstats(PrepArgs a) {
+  const int j = blockIdx.x, bh = blockIdx.y, p = threadIdx.x;
   const int r0 = j * BLK;
   const int valid = min(BLK, a.N - r0);
   const size_t head = (size_t)bh * a.N;
-
-  if (wave == 0) {
+  {
+    // keys: lane p sums channels (2p, 2p+1) of the rotated rows in ascending order (sequential fp32
+    // sums from 0); rows are read 32 at a time, each row one 256-byte segment across the wave
     if (!a.smooth_k) return;
-    const uint32_t* K = reinterpret_cast<const uint32_t*>(a.K) + head * 64 + p;
+    const uint32_t* Kp = reinterpret_cast<const uint32_t*>(a.K) + head * 64 + p;
+    const int ax = rope_axis(p);
     float s0 = 0.f, s1 = 0.f;
     for (int r = 0; r < valid; r += 32) {
       uint32_t w[32];
+      float c[32], sn[32];
 #pragma unroll
-      for (int u = 0; u < 32; ++u) w[u] = (r + u < valid) ? K[(size_t)(r0 + r + u) * 64] : 0u;
+      for (int u = 0; u < 32; ++u) {
+        const bool in = r + u < valid;
+        w[u] = in ? Kp[(size_t)(r0 + r + u) * 64] : 0u;
+        if (a.rope) {
+          const RopeRows rr = rope_rows(in ? r0 + r + u : r0, a);
+          const int row = ax == 0 ? rr.f : (ax == 1 ? rr.y : rr.x);
+          c[u] = a.rope_cos[row * 64 + p];
+          sn[u] = a.rope_sin[row * 64 + p];
+        }
+      }
 #pragma unroll
       for (int u = 0; u < 32; ++u) {
         if (r + u < valid) {
-          float x0 = bf16_lo(w[u]), x1 = bf16_hi(w[u]);
-          if (a.rope) rope_pair(x0, x1, p, r0 + r + u, a);
-          s0 = s0 + x0;
-          s1 = s1 + x1;
+          float y0 = bf16_lo(w[u]), y1 = bf16_hi(w[u]);
+          if (a.rope) {
+            const float x0 = y0, x1 = y1;
+            const float pp = x1 * sn[u], qq = x1 * c[u];
+            y0 = __builtin_fmaf(x0, c[u], -pp);
+            y1 = __builtin_fmaf(x0, sn[u], qq);
+          }
+          s0 = s0 + y0;
+          s1 = s1 + y1;
         }
       }
     }
     float* out = a.ws_ksum + ((size_t)bh * a.T + j) * D + 2 * p;
     out[0] = s0;
     out[1] = s1;
-  } else {
-    const uint32_t* V = reinterpret_cast<const uint32_t*>(a.V) + head * 64 + p;
+  }
+}
+
+__global__ __launch_bounds__(64) void prep_vstats(PrepArgs a) {
+  const int j = blockIdx.x, bh = blockIdx.y, p = threadIdx.x;
+  const int r0 = j * BLK;
+  const int valid = min(BLK, a.N - r0);
+  const size_t head = (size_t)bh * a.N;
+  {
+    // values: the gathered rows of permuted block j, 32 at a time; the second pass (a max, any
+    // order) reads them again (from the cache)
+    const uint32_t* Vp = reinterpret_cast<const uint32_t*>(a.V) + head * 64 + p;
     const int32_t* perm = a.perm ? a.perm + head : nullptr;
+    auto load32 = [&](int r, uint32_t (&w)[32]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < 32; ++u) {
+        const int row = min(r0 + r + u, a.N - 1);
+        const int n = perm ? clamp_index(perm[row], a.N) : row;
+        w[u] = r + u < valid ? Vp[(size_t)n * 64] : 0u;
+      }
+    };
     float s0 = 0.f, s1 = 0.f;
     for (int r = 0; r < valid; r += 32) {
       uint32_t w[32];
+      load32(r, w);
 #pragma unroll
-      for (int u = 0; u < 32; ++u) {
-        const int row = r0 + r + u;
-        const int n = perm ? clamp_index(perm[min(row, a.N - 1)], a.N) : row;
-        w[u] = (r + u < valid) ? V[(size_t)n * 64] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < 32; ++u) {
+      for (int u = 0; u < 32; ++u)
         if (r + u < valid) {
-          vrows[r + u][p] = w[u];
           s0 = s0 + bf16_lo(w[u]);
           s1 = s1 + bf16_hi(w[u]);
         }
-      }
     }
     float mu0 = 0.f, mu1 = 0.f;
     uint16_t* mean_out = a.v_mean + ((size_t)bh * a.T + j) * D + 2 * p;
@@ -99,10 +155,15 @@ __global__ __launch_bounds__(128) void prep_stats(PrepArgs a) {
       mean_out[1] = 0;
     }
     float m0 = 0.f, m1 = 0.f;
-    for (int r = 0; r < valid; ++r) {  // same wave wrote vrows: no barrier needed
-      const uint32_t w = vrows[r][p];
-      m0 = fmaxf(m0, fabsf(bf16_lo(w) - mu0));
-      m1 = fmaxf(m1, fabsf(bf16_hi(w) - mu1));
+    for (int r = 0; r < valid; r += 32) {
+      uint32_t w[32];
+      load32(r, w);
+#pragma unroll
+      for (int u = 0; u < 32; ++u)
+        if (r + u < valid) {
+          m0 = fmaxf(m0, fabsf(bf16_lo(w[u]) - mu0));
+          m1 = fmaxf(m1, fabsf(bf16_hi(w[u]) - mu1));
+        }
     }
     float* out = a.ws_vamax + ((size_t)bh * a.T + j) * D + 2 * p;
     out[0] = m0;
@@ -120,12 +181,12 @@ __global__ __launch_bounds__(128) void prep_finalize(PrepArgs a) {
   if (a.smooth_k) {
     const float* part = a.ws_ksum + (size_t)bh * a.T * D + c;
     float tot = 0.f;
-    for (int j0 = 0; j0 < a.T; j0 += 16) {   // sequential sum over blocks; loads issued 16 ahead
-      float v[16];
+    for (int j0 = 0; j0 < a.T; j0 += 64) {   // sequential sum over blocks; loads issued 64 ahead
+      float v[64];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = part[(size_t)min(j0 + u, a.T - 1) * D];
+      for (int u = 0; u < 64; ++u) v[u] = part[(size_t)min(j0 + u, a.T - 1) * D];
 #pragma unroll
-      for (int u = 0; u < 16; ++u)
+      for (int u = 0; u < 64; ++u)
         if (j0 + u < a.T) tot = tot + v[u];
     }
     km = tot / (float)a.N;
@@ -133,12 +194,12 @@ __global__ __launch_bounds__(128) void prep_finalize(PrepArgs a) {
   a.k_mean[(size_t)bh * D + c] = km;
   const float* am = a.ws_vamax + (size_t)bh * a.T * D + c;
   float amax = 0.f;
-  for (int j0 = 0; j0 < a.T; j0 += 16) {
-    float v[16];
+  for (int j0 = 0; j0 < a.T; j0 += 64) {
+    float v[64];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) v[u] = am[(size_t)min(j0 + u, a.T - 1) * D];
+    for (int u = 0; u < 64; ++u) v[u] = am[(size_t)min(j0 + u, a.T - 1) * D];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) amax = fmaxf(amax, v[u]);
+    for (int u = 0; u < 64; ++u) amax = fmaxf(amax, v[u]);
   }
   a.v_scale[(size_t)bh * D + c] = amax > 0.f ? amax / 448.f : 1.f;
   a.ws_vinv[(size_t)bh * D + c] = amax > 0.f ? 448.f / amax : 0.f;
@@ -170,17 +231,22 @@ __device__ __forceinline__ void fwht_rows(float (&x)[4][8], int k4) {
           x[i][e + h] = lo - hi;
         }
   // bits 3, 4: k4, across lanes (xor 1, xor 2)
-#pragma unroll
-  for (int m = 1; m <= 2; m <<= 1) {
-    const bool upper = (k4 & m) != 0;
+  // lane ^ 1 and lane ^ 2 inside the quad (quad_perm [1,0,3,2] and [2,3,0,1]): the lower lane
+  // of a pair keeps own + other, the upper lane other - own = other + (-own)
+  auto cross = [&](auto CTRL, bool upper) __attribute__((always_inline)) {
+    const float sgn = upper ? -1.f : 1.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float own = x[i][e], other = __shfl_xor(own, m);
-        x[i][e] = upper ? other - own : own + other;
+        const float own = x[i][e];
+        const float other =
+            __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, own), decltype(CTRL)::value, 0xf, 0xf, false));
+        x[i][e] = other + own * sgn;
       }
-  }
+  };
+  cross(std::integral_constant<int, 0xb1>{}, (k4 & 1) != 0);
+  cross(std::integral_constant<int, 0x4e>{}, (k4 & 2) != 0);
   // bits 5, 6: i, inside the lane
 #pragma unroll
   for (int h = 1; h < 4; h <<= 1)
@@ -227,11 +293,38 @@ __global__ __launch_bounds__(256) void prep_quant(PrepArgs a) {
     const int n = valid[it] ? (gather ? clamp_index(gather[row], a.N) : row) : 0;
     load_row32(X + (head + n) * D, k4, x[it]);
     if (z < 2) {
-      if (a.rope)
+      if (a.rope) {
+        const RopeRows rr = rope_rows(n, a);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i) {
+          // pairs 16i + 4k4 .. +3: one 16-byte load per table from the row of the first pair's
+          // axis; the two quads that cross an axis boundary (pairs 20..23 and 40..43) patch the
+          // pairs of the next axis
+          const int p0 = 16 * i + 4 * k4;
+          const int ax0 = rope_axis(p0);
+          const int row = ax0 == 0 ? rr.f : (ax0 == 1 ? rr.y : rr.x);
+          float4 c4 = *reinterpret_cast<const float4*>(a.rope_cos + row * 64 + p0);
+          float4 s4 = *reinterpret_cast<const float4*>(a.rope_sin + row * 64 + p0);
+          if (i == 1 && k4 == 1) {
+            c4.z = a.rope_cos[rr.y * 64 + 22];
+            c4.w = a.rope_cos[rr.y * 64 + 23];
+            s4.z = a.rope_sin[rr.y * 64 + 22];
+            s4.w = a.rope_sin[rr.y * 64 + 23];
+          }
+          if (i == 2 && k4 == 2) {
+            c4.w = a.rope_cos[rr.x * 64 + 43];
+            s4.w = a.rope_sin[rr.x * 64 + 43];
+          }
+          const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-          for (int e = 0; e < 8; e += 2) rope_pair(x[it][i][e], x[it][i][e + 1], 16 * i + 4 * k4 + e / 2, n, a);
+          for (int e = 0; e < 8; e += 2) {
+            const float x0 = x[it][i][e], x1 = x[it][i][e + 1];
+            const float pp = x1 * ss[e / 2], qq = x1 * cc[e / 2];
+            x[it][i][e] = __builtin_fmaf(x0, cc[e / 2], -pp);
+            x[it][i][e + 1] = __builtin_fmaf(x0, ss[e / 2], qq);
+          }
+        }
+      }
       if (z == 1 && a.smooth_k) {
         const float* km = a.k_mean + (size_t)bh * D;
 #pragma unroll
@@ -325,7 +418,8 @@ __global__ __launch_bounds__(256) void prep_quant(PrepArgs a) {
 }
 
 hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
-  prep_stats<<<dim3(a.T, BH), 128, 0, s>>>(a);
+  if (a.smooth_k) prep_kstats<<<dim3(a.T, BH), 64, 0, s>>>(a);
+  prep_vstats<<<dim3(a.T, BH), 64, 0, s>>>(a);
   prep_finalize<<<dim3(BH), 128, 0, s>>>(a);
   prep_quant<<<dim3(a.T, BH, 3), 256, 0, s>>>(a);
   return hipGetLastError();

@@ -21,6 +21,7 @@ struct PrepArgs {
   float* ws_vamax;  // [B*H][T][128] per-block residual maxima
   float* ws_vinv;   // [B*H][128]    448 / amax (0 for an all-zero channel)
   int N, T, F, Ht, Wd;
+  float inv_w, inv_hw;  // 1/Wd and 1/(Ht*Wd) in fp32: estimates for the token-position divisions
   int rope, hadamard, smooth_k, smooth_v;
 };
 
