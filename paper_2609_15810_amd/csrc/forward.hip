@@ -7,34 +7,36 @@
 //                         in registers for the whole kernel);
 //   O^T += V_hat^T P^T    FP8 MFMA 32x32x64 (A = residual codes from LDS, B = P codes).
 // A lane's 16 results of a 32-key block are 16 keys of its own query, so the running row maximum
-// is an in-register max plus one exchange with lane l^32, alpha and l are per-lane scalars, and the
-// ExpCast-FP8 codes are already in the B-operand order of the FP8 product: byte s of lane half kh
-// in key chunk kc is key 32(2kc + s/16) + 8((s%16)/4) + 4kh + s%4, the order in which the
-// preprocessing stores V_hat.
+// is an in-register max plus one exchange with lane l^32 (v_permlane32_swap), alpha and l are
+// per-lane scalars, and the ExpCast-FP8 codes are already in the B-operand order of the FP8
+// product: byte s of lane half kh in key chunk kc is key 32(2kc + s/16) + 8((s%16)/4) + 4kh + s%4,
+// the order in which the preprocessing stores V_hat.
 //
-// Ping-pong schedule. Each wave alternates a matrix phase M_j (value product and row sum of tile j,
-// scores of tile j+1) and a vector phase V_j (running maximum, rescale and ExpCast codes of tile j).
-// Waves 4..7 run one phase behind waves 0..3 and every phase ends at a workgroup barrier; waves w
-// and w+4 share a SIMD, so on every SIMD one wave feeds the matrix cores while the other runs the
-// softmax on the vector ALU.
+// Software pipeline inside each wave. Iteration j issues the value product of tile j (its codes
+// were formed in iteration j-1), forms the running maximum and the codes of tile j+1, and issues
+// the scores of tile j+2, in regions that each pair matrix work with vector work of about the same
+// length (scheduling barriers keep the regions in order; the codes of key block kb of tile j+1
+// are formed before the scores of block kb of tile j+2 overwrite its registers). The matrix cores
+// thus run the value and score products of one wave while its vector ALU forms codes; the two
+// waves of a SIMD share both.
 //
 // Per score the vector ALU does one int-to-float conversion, one fp32 fma and one
 // round-to-nearest-even saturating byte conversion (the code is the one-rounding
 // fma(float(acc), 8a, fl(fl(120 + beta) - 8m')) of the method's fp32 formula), plus half a max3.
-// The probability row sum r_j is an all-ones E4M3 A operand times the P codes. Block means are
-// restored in batches of 8 tiles: (r_j, m_j) is kept in LDS, and every 8 tiles
-// O^T += M^T R with R_t = r_t 2^(m_t - m) is one bf16 matrix product pair (mu_t / s_V and R split
-// into hi + lo bf16 parts, relative error ~2^-16). The rescale by alpha is skipped when no row
-// maximum of the wave moved.
+// The probability row sum r_j is one FP8 16x16x128 product per 64 keys whose A operand holds ones
+// only in rows 0, 4, 8 and 12 (so that lane l receives r of its own query). Block means are
+// restored in batches of 8 tiles: (r_j, m_j) is kept in LDS, and every 8 tiles O^T += M^T R with
+// R_t = r_t 2^(m_t - m) is one bf16 matrix product pair (mu_t / s_V and R split into hi + lo bf16
+// parts, relative error ~2^-16). The rescale by alpha is skipped when no row maximum of the wave
+// moved.
 //
-// Tiles go straight from memory into LDS (16 KB of K_hat, 16 KB of V_hat per tile, four buffers),
-// issued as asm so that the compiler adds no waits of its own: each wave waits (vmcnt) for its own
-// share of a tile pair before the barrier that precedes the pair's first use, and the copies of
-// the next two pairs stay in flight. Half of V_j's operands are read into registers at the end of
-// V_j, when the LDS port of that wave is otherwise idle. The steady-state loop is unrolled by four
-// tiles so that every LDS access names its buffer statically. Tiles are visited in ascending order
-// with the running maximum updated once per 128-key tile, the schedule on which the codes are
-// defined.
+// Tiles go straight from memory into LDS (16 KB of K_hat, 16 KB of V_hat per tile, four buffers
+// each), issued as asm so that the compiler adds no waits of its own: pair p = (K_{p+2}, V_p with
+// its block means) is copied during iteration p-3, each wave waits (vmcnt) for its own share of
+// pair p+1 before the barrier that ends iteration p, and the next two pairs stay in flight. The
+// steady-state loop is unrolled by four iterations so that every LDS access names its buffer
+// statically. Tiles are visited in ascending order with the running maximum updated once per
+// 128-key tile, the schedule on which the codes are defined.
 #include <type_traits>
 
 #include "vc_common.hpp"
@@ -44,23 +46,41 @@
 
 namespace vc {
 
-constexpr int FWD_WAVES = 8;
-constexpr int FWD_THREADS = 64 * FWD_WAVES;
-constexpr int FWD_QUERIES = 32 * FWD_WAVES;  // 256: two query blocks
-constexpr int TILE_BYTES = BLK * D;          // 16384
-constexpr int VBUF_BYTES = TILE_BYTES + 2 * D;  // V tile, then its 128 bf16 means
-// s_waitcnt immediates (vmcnt in bits 3:0 and 15:14, the other counters left at their maxima)
-constexpr int WAIT_VM0 = 0x3f70;
-constexpr int WAIT_VM_PAIR = 0x3f75;    // vmcnt(5): the five copies of one pair may remain
-constexpr int WAIT_VM_2PAIRS = 0x3f7a;  // vmcnt(10): the copies of two pairs may remain
+constexpr int NW = 8;             // waves per workgroup, 32 queries each (two per SIMD)
+constexpr int NTH = 64 * NW;
+constexpr int NQ = 32 * NW;
+constexpr int TILE_BYTES = BLK * D;
+constexpr int VBUF_BYTES = TILE_BYTES + 2 * D;
+constexpr int KCOPIES = TILE_BYTES / 1024 / NW;  // 1 KB copies per wave per tile
+constexpr int PAIR_COPIES = 2 * KCOPIES + 1;     // K and V pieces + the means
+constexpr int MEAN_LANES = 64 / NW;              // lanes copying 4 bytes of means each
+
+// s_waitcnt immediate for vmcnt(n) (bits 3:0 and 15:14), the other counters left at their maxima
+constexpr int vm_wait(int n) { return 0x3f70 | (n & 0xf) | ((n >> 4) << 14); }
+// wait until at most n pairs' copies of this wave are in flight
+__device__ __forceinline__ void wait_pairs(int n) {
+  if (n >= 2) __builtin_amdgcn_s_waitcnt(vm_wait(2 * PAIR_COPIES));
+  else if (n == 1) __builtin_amdgcn_s_waitcnt(vm_wait(PAIR_COPIES));
+  else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
   return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ v16f mfma_f8(v8i a, v8i b, v16f c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+__device__ __forceinline__ v4f mfma_f8_16(v8i a, v8i b, v4f c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// max of v over lanes l and l^32 (the two key halves of a query)
+__device__ __forceinline__ int half_max(int v) {
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return max(max(v, (int)r[0]), (int)r[1]);
 }
 
 // Copies from global memory straight into LDS: lane l moves `bytes` bytes from base + voff to
@@ -79,11 +99,10 @@ __device__ __forceinline__ void copy4_to_lds(const void* base, uint32_t voff, ui
                : "memory", "m0");
 }
 
-// Workgroup barrier for the phase schedule. The wave's own LDS stores are complete before it
-// (lgkmcnt(0)); the tile copies into LDS are waited for explicitly (vmcnt) by the caller, so the
-// copies issued for later tiles stay in flight across it. The empty asm statements keep the
-// compiler from moving memory accesses across, the scheduling barriers keep it from moving
-// anything across.
+// Workgroup barrier. The wave's own LDS stores are complete before it (lgkmcnt(0)); the tile
+// copies into LDS are waited for explicitly (vmcnt) by the caller, so the copies issued for later
+// tiles stay in flight across it. The empty asm statements keep the compiler from moving memory
+// accesses across, the scheduling barriers keep it from moving anything across.
 __device__ __forceinline__ void wg_barrier() {
   __builtin_amdgcn_s_waitcnt(0xc07f);
   asm volatile("" ::: "memory");
@@ -93,8 +112,8 @@ __device__ __forceinline__ void wg_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Empty asm that reads and rewrites x: values computed in a phase stay in that phase (the compiler
-// may not sink their computation past the barrier that ends it).
+// Empty asm that reads and rewrites x: x is formed before this point (a pure value would
+// otherwise be computed next to its first use).
 template <typename V>
 __device__ __forceinline__ void pin(V& x) {
   asm volatile("" : "+v"(x));
@@ -125,16 +144,10 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
-// wait until at most n pairs' copies (5 each) of this wave are in flight
-__device__ __forceinline__ void wait_pairs(int n) {
-  if (n >= 2) __builtin_amdgcn_s_waitcnt(WAIT_VM_2PAIRS);
-  else if (n == 1) __builtin_amdgcn_s_waitcnt(WAIT_VM_PAIR);
-  else __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-}
-
 template <int PMODE>
-__global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd(FwdArgs a) {
-  // four tile buffers: K_0 in buffer 0, pair p = (K_{p+1}, V_p with its block means) in buffer (p+1) mod 4
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_fwd(FwdArgs a) {
+  // K_t in kb[t % 4]; V_t with its 128 bf16 block means in vb[t % 4]; mu_t / s_V as bf16 hi + lo
+  // in slot t % 8 of ub[(t / 8) % 2]; (r_t, m_t) per query in slot t % 8 of rm[wave]
   __shared__ __attribute__((aligned(16))) uint8_t kb0[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t kb1[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t kb2[TILE_BYTES];
@@ -143,25 +156,24 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   __shared__ __attribute__((aligned(16))) uint8_t vb1[VBUF_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t vb2[VBUF_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t vb3[VBUF_BYTES];
-  __shared__ __attribute__((aligned(16))) uint16_t ub[2][2][D][8];        // [chunk parity][hi, lo][channel][slot]
-  __shared__ __attribute__((aligned(16))) float2 rm[FWD_WAVES][32][8];   // (r_t, m_t) per query, slot t % 8
+  __shared__ __attribute__((aligned(16))) uint16_t ub[2][2][D][8];
+  __shared__ __attribute__((aligned(16))) float2 rm[NW][32][8];
   __shared__ float svs[D], inv_svs[D];
 
   const int qt = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kh = lane >> 5, col = lane & 31;
-  const bool lead = wave < FWD_WAVES / 2;  // waves 0..3 lead, 4..7 (same SIMDs) follow one phase behind
   const int T = a.T;
   const size_t tile0 = (size_t)bh * T;
 
-  // the wave's 32 queries (query block 2 qt + wave / 4, rows 32 (wave % 4) ..) as the B operand
-  const int qblock = min(2 * qt + (wave >> 2), T - 1);
+  const int gq = NW * qt + wave;  // global 32-query group
+  const int qblock = min(gq >> 2, T - 1);
   const int8_t* qblk = a.q + (tile0 + qblock) * TILE_BYTES;
   v4i qop[4];
 #pragma unroll
   for (int dc = 0; dc < 4; ++dc)
-    qop[dc] = *reinterpret_cast<const v4i*>(qblk + (((wave & 3) * 4 + dc) * 2 + kh) * 512 + col * 16);
+    qop[dc] = *reinterpret_cast<const v4i*>(qblk + (((gq & 3) * 4 + dc) * 2 + kh) * 512 + col * 16);
   const float sq = a.q_scale[tile0 + qblock];
 
   const int mc = tid & (D - 1);
@@ -170,41 +182,50 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     svs[tid] = sv;
     inv_svs[tid] = 1.f / sv;
   }
-  reinterpret_cast<u4*>(&ub[0][0][0][0])[tid] = u4{0, 0, 0, 0};  // 512 x 16 B: the whole array
+  for (int e = tid; e < 2 * 2 * D * 8 / 8; e += NTH) reinterpret_cast<u4*>(&ub[0][0][0][0])[e] = u4{0, 0, 0, 0};
+
+  // row-sum operand of the 16x16x128 FP8 product: A rows 0 and 8 are ones on k-groups 0 and 2
+  // (B lanes 0..15 and 32..47: queries 0..15), rows 4 and 12 on k-groups 1 and 3 (queries
+  // 16..31); C row 4(l/16), column l%16 then holds r of query l%32 in register 0 of lane l
+  v8i ones16;
+  {
+    const int row = lane & 15, g = lane >> 4;
+    const bool on = ((row == 0 || row == 8) && !(g & 1)) || ((row == 4 || row == 12) && (g & 1));
+    const int w = on ? 0x38383838 : 0;
+    ones16 = v8i{w, w, w, w, w, w, w, w};
+  }
 
   const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + tile0 * TILE_BYTES;
   const uint8_t* vbase = a.v + tile0 * TILE_BYTES;
-  const uint8_t* mbase = reinterpret_cast<const uint8_t*>(a.v_mean + tile0 * D) + 32 * wave;
-  // K_0: two 1 KB copies per wave
-  auto load_k0 = [&]() __attribute__((always_inline)) {
+  const uint8_t* mbase = reinterpret_cast<const uint8_t*>(a.v_mean + tile0 * D) + (2 * D / NW) * wave;
+  // K_t into kd: KCOPIES 1 KB copies per wave
+  auto load_k = [&](int t, uint8_t* kd) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int off = (u * FWD_WAVES + wave) * 1024;
-      copy16_to_lds(kbase + off, lane * 16, lds_addr(kb0 + off));
+    for (int u = 0; u < KCOPIES; ++u) {
+      const int off = (u * NW + wave) * 1024;
+      copy16_to_lds(kbase + (size_t)t * TILE_BYTES + off, lane * 16, lds_addr(kd + off));
     }
   };
-  // copy k (0..4) of pair p: two 1 KB pieces of K_{p+1} (clamped to the last tile), two of V_p,
-  // 32 bytes of V_p's means. Every wave issues exactly five copies per pair, the number the
-  // waits count.
+  // copy k of pair p = (K_{p+2} clamped to the last tile, V_p with its means)
   auto load_part = [&](int k, int p, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
-    if (k < 4) {
-      const uint8_t* src = k < 2 ? kbase + (size_t)min(p + 1, T - 1) * TILE_BYTES : vbase + (size_t)p * TILE_BYTES;
-      uint8_t* dst = k < 2 ? kd : vd;
-      const int off = ((k & 1) * FWD_WAVES + wave) * 1024;
+    if (k < 2 * KCOPIES) {
+      const bool isk = k < KCOPIES;
+      const uint8_t* src = isk ? kbase + (size_t)min(p + 2, T - 1) * TILE_BYTES : vbase + (size_t)p * TILE_BYTES;
+      uint8_t* dst = isk ? kd : vd;
+      const int off = ((isk ? k : k - KCOPIES) * NW + wave) * 1024;
       copy16_to_lds(src + off, lane * 16, lds_addr(dst + off));
-    } else if (lane < 8) {
-      copy4_to_lds(mbase + (size_t)p * 2 * D, 4 * lane, lds_addr(vd + TILE_BYTES + 32 * wave));
+    } else if (lane < MEAN_LANES) {
+      copy4_to_lds(mbase + (size_t)p * 2 * D, 4 * lane, lds_addr(vd + TILE_BYTES + (2 * D / NW) * wave));
     }
   };
   auto load_pair = [&](int p, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
 #pragma unroll
-    for (int k = 0; k < 5; ++k) load_part(k, p, kd, vd);
+    for (int k = 0; k < PAIR_COPIES; ++k) load_part(k, p, kd, vd);
   };
-  // K scales through the scalar cache
   const __attribute__((address_space(4))) float* kscale =
       (const __attribute__((address_space(4))) float*)(a.k_scale + tile0);
   // mu_j / s_V as bf16 hi + lo into slot j % 8 of chunk parity (j / 8) % 2, from the means behind
-  // V_j in vt (leaders only: threads 128..255 store the same values as threads 0..127)
+  // V_j in vt (threads 0..127, one channel each)
   auto stash_mean = [&](int j, const uint8_t* vt) __attribute__((always_inline)) {
     if (a.smooth_v) {
       const float u = bf16_to_f32(reinterpret_cast<const uint16_t*>(vt + TILE_BYTES)[mc]) * inv_svs[mc];
@@ -220,13 +241,9 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  const v8i ones = {0x38383838, 0x38383838, 0x38383838, 0x38383838, 0x38383838, 0x38383838, 0x38383838, 0x38383838};
-  // s: scores of the tile whose codes are computed next; after the vector phase s[0] holds that
-  // tile's ExpCast codes (the two v8i B operands of the value product)
-  v16i s[4];
-  v8i vops[4];              // first half of the V_j operands, read at the end of V_j for M_j
-  float rsum = 0.f;         // row sum of the tile whose value product was issued last
-  float ksc = 0.f;          // scale of the K tile whose scores are in s
+  v16i s[4];       // scores of the tile whose codes are computed next
+  v8i pc[2];       // codes of the tile whose value product is issued next
+  float ksc = 0.f;  // scale of the K tile whose scores are in s
   float2* rm_q = &rm[wave][col][0];
 
   // O^T += M^T R for the tiles of chunk parity `par` whose slot is <= last_slot, R_t = r_t 2^(m_t - m)
@@ -251,14 +268,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
   };
 
-  // r of tile jp (computed by the matrix phase before, at the running maximum m_run) into l and
-  // slot jp % 8 of (r, m)
-  auto fold_rowsum = [&](int jp) __attribute__((always_inline)) {
-    l_run += rsum;
-    rm_q[jp & 7] = make_float2(rsum, m_run);
-  };
-
-  // V_j operand n of the value product (A operand: residual codes, 32 channels x 64 keys)
+  // value operand n of tile vt (A operand: residual codes, 32 channels x 64 keys; n = 4 kc + db)
   auto load_vop = [&](const uint8_t* vt, int n) __attribute__((always_inline)) -> v8i {
     const int kc = n >> 2, db = n & 3;
     const int base = ((((kc * 4 + db) * 2 + kh) * 2) * 32 + col) * 16;
@@ -266,81 +276,25 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     const u4 hi = *reinterpret_cast<const u4*>(vt + base + 512);
     return v8i{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
   };
-  auto prefetch_v = [&](const uint8_t* vt) __attribute__((always_inline)) {
-    __builtin_amdgcn_sched_barrier(0);  // after the codes: the scores' registers are free by then
+
+  // scores of tile t (K_t in kt) into s
+  auto qk = [&](auto MASKC, int t, const uint8_t* kt) __attribute__((always_inline)) {
+    ksc = kscale[t];
 #pragma unroll
-    for (int n = 0; n < 4; ++n) vops[n] = load_vop(vt, n);
+    for (int kb = 0; kb < 4; ++kb) {
+      v4i kops[4];
+#pragma unroll
+      for (int dc = 0; dc < 4; ++dc) kops[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
+      v16i acc = {};
+#pragma unroll
+      for (int dc = 0; dc < 4; ++dc) acc = mfma_i8(kops[dc], qop[dc], acc);
+      s[kb] = acc;
+    }
+    if (decltype(MASKC)::value) mask_tile(s, kh, a.N - (T - 1) * BLK);
   };
 
-  // matrix phase M_j: value product and row sum of tile j (codes in s[0], operands in vops), scores
-  // of tile j+1 (K_{j+1} in kt, read two pieces behind each value product), then the means of chunk
-  // j/8 - 1 once j is a multiple of 8. hook(n), n = 0..4, issues copy n of a later pair between the
-  // products. PVC / QKC / MASKC (std::integral_constant): value product, scores, ragged tile j+1.
-  auto mphase_m = [&](auto PVC, auto QKC, auto MASKC, int j, const uint8_t* kt, const uint8_t* vt, auto hook) __attribute__((always_inline)) {
-    constexpr bool pv = decltype(PVC)::value, qk = decltype(QKC)::value;
-    v4i kops[16];
-    auto load_k = [&](int n) __attribute__((always_inline)) {
-      const int dc = n >> 2, kb = n & 3;
-      kops[n] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
-    };
-    if (pv) {
-      const v8i p0 = __builtin_shufflevector(s[0], s[0], 0, 1, 2, 3, 4, 5, 6, 7);
-      const v8i p1 = __builtin_shufflevector(s[0], s[0], 8, 9, 10, 11, 12, 13, 14, 15);
-      v8i vops2[4];
-#pragma unroll
-      for (int n = 0; n < 4; ++n) vops2[n] = load_vop(vt, 4 + n);
-      v16f rs = {};
-      rs = mfma_f8(ones, p0, rs);
-      rs = mfma_f8(ones, p1, rs);
-#pragma unroll
-      for (int n = 0; n < 8; ++n) {
-        const int kc = n >> 2, db = n & 3;
-        o[db] = mfma_f8(n < 4 ? vops[n] : vops2[n - 4], kc == 0 ? p0 : p1, o[db]);
-        if (qk) {
-          load_k(2 * n);
-          load_k(2 * n + 1);
-        }
-        if (n < 5) hook(n);
-      }
-      rsum = rs[0];
-    } else {
-#pragma unroll
-      for (int n = 0; n < 16; ++n) {
-        if (qk) load_k(n);
-        if (n < 5) hook(n);
-      }
-    }
-    if (qk) {
-      ksc = kscale[j + 1];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] = 0;
-#pragma unroll
-      for (int n = 0; n < 16; ++n) {
-        const int dc = n >> 2, kb = n & 3;
-        s[kb] = mfma_i8(kops[n], qop[dc], s[kb]);
-      }
-      if (decltype(MASKC)::value) mask_tile(s, kh, a.N - (T - 1) * BLK);
-    }
-    if (pv && qk) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-#pragma unroll
-      for (int n = 0; n < 8; ++n) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-    }
-    if (pv && a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
-  };
-
-  // vector phase V_j: fold r_{j-1}; running maximum and alpha of tile j; rescale; codes of tile j
-  // into s[0]. LASTC (std::integral_constant): tile j is the ragged last tile.
-  auto vphase = [&](auto LASTC, int j) __attribute__((always_inline)) {
-    constexpr bool last = decltype(LASTC)::value;
-    if (j >= 1) fold_rowsum(j - 1);
+  // running maximum of tile t (scores in s) into m_new, alpha, codes into pn
+  auto softmax = [&](auto LASTC, int t, v8i (&pn)[2], float& alpha, float& m_new) __attribute__((always_inline)) {
     const float a_s = (sq * ksc) * a.kappa;  // the oracle's order: fl(fl(s_q s_k) kappa)
     int mk[4];
 #pragma unroll
@@ -351,20 +305,11 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       mk[kb] = m;
     }
     int mx = max(max(mk[0], mk[1]), max(mk[2], mk[3]));
-    mx = max(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, (float)mx * a_s);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      l_run *= alpha;
-    }
+    mx = half_max(mx);
+    m_new = fmaxf(m_run, (float)mx * a_s);
+    alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     const float a8 = 8.f * a_s;
     const float bias = a.cbias - 8.f * m_new;
-    v8i p[2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -381,142 +326,278 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
           w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(pe[0], pe[1], 0, false);
           w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(pe[2], pe[3], (int)w, true);
         }
-        p[kb >> 1][4 * (kb & 1) + d4] = (int)w;
+        pn[kb >> 1][4 * (kb & 1) + d4] = (int)w;
       }
-    if (last) clear_padded(p, kh, a.N - j * BLK);
-    s[0] = __builtin_shufflevector(p[0], p[1], 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+    if (decltype(LASTC)::value) clear_padded(pn, kh, a.N - t * BLK);
   };
 
   const std::integral_constant<bool, false> NO;
   const std::integral_constant<bool, true> YES;
-  auto nohook = [](int) {};
 
-  // end of a phase: the phase's results are final before the workgroup barrier, and the next
-  // phase's work starts after it
   auto pin_state = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < 4; ++db) pin(o[db]);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) pin(s[kb]);
+    pin(pc[0]);
+    pin(pc[1]);
     pin(l_run);
     pin(m_run);
-    pin(rsum);
     pin(ksc);
   };
-  // wait: -1 none, else the number of this wave's pairs that may stay in flight
-  auto end_phase = [&](int wait) __attribute__((always_inline)) {
+  auto end_iter = [&](int npairs) __attribute__((always_inline)) {
     pin_state();
-    if (wait >= 0) wait_pairs(wait);
+    wait_pairs(npairs);
     wg_barrier();
     pin_state();
   };
 
-  // Every wave runs the phase sequence M_{-1}, V_0, M_0, V_1, ..., V_{T-1}, M_{T-1}, F with a
-  // barrier after each phase; the followers pass one extra barrier before their first phase and
-  // the leaders one after their last, so a follower's phase k meets a leader's phase k+1 (global
-  // phase 2j+1 holds the leaders' V_j and the followers' M_{j-1}). Pair p is read from global
-  // phase 2p+1 on (the leaders' V_p reads V_p's operands and means, M_p reads K_{p+1}) until 2p+3,
-  // so it must have landed in every wave's share by the barrier ending global phase 2p: the leaders
-  // wait after M_{p-1}, the followers after V_{p-1}. A wave issues its share of pair p during its
-  // M_{p-3}, between the value products; the pair's buffer was last read by pair p-4 in global
-  // phase 2p-5.
+  // iteration j: value product and row sum of tile j (codes pc, V_j in vt); codes of tile j+1
+  // (SOFTC; LASTC: it is the ragged last tile); scores of tile j+2 (QKC, K_{j+2} in kt; MASKC:
+  // the last tile); pair j+3 copied into (kd, vd) (COPYC); mean j stashed; rescale to m_{j+1}
+  auto iter = [&](auto COPYC, auto SOFTC, auto QKC, auto MASKC, auto LASTC, int j, const uint8_t* vt,
+                  const uint8_t* kt, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
+    constexpr bool cp = decltype(COPYC)::value, soft = decltype(SOFTC)::value, doqk = decltype(QKC)::value;
+    v8i vop[8];
+#pragma unroll
+    for (int n = 0; n < 8; ++n) vop[n] = load_vop(vt, n);
+    v4f rs = {};
+    rs = mfma_f8_16(ones16, pc[0], rs);
+    rs = mfma_f8_16(ones16, pc[1], rs);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      o[n & 3] = mfma_f8(vop[n], pc[n >> 2], o[n & 3]);
+      if (cp && n < PAIR_COPIES) load_part(n, j + 3, kd, vd);
+    }
+    if (cp)
+#pragma unroll
+      for (int k = 8; k < PAIR_COPIES; ++k) load_part(k, j + 3, kd, vd);
+    v8i pn[2];
+    float alpha = 1.f, m_new = m_run;
+    if (soft) softmax(LASTC, j + 1, pn, alpha, m_new);
+    if (doqk) qk(MASKC, j + 2, kt);
+    const float rsum = rs[0];
+    if (a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
+    rm_q[j & 7] = make_float2(rsum, m_run);
+    l_run += rsum;
+    if (tid < D) stash_mean(j, vt);
+    if (soft) {
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        l_run *= alpha;
+      }
+      m_run = m_new;
+      pc[0] = pn[0];
+      pc[1] = pn[1];
+    }
+    end_iter(cp ? 2 : 0);
+  };
+
+  // steady-state iteration j (codes of tile j+1 and scores of tile j+2 exist, neither is the last
+  // tile), issued in regions that each pair matrix work with vector work of about the same
+  // length; the scheduling barriers keep the regions in this order, so the scores of key block
+  // kb of tile j+2 are written only after the codes of key block kb of tile j+1 are formed
+  auto fence = []() __attribute__((always_inline)) { __builtin_amdgcn_sched_barrier(0); };
+  auto iter_fast = [&](auto COPYC, int j, const uint8_t* vt, const uint8_t* kt, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
+    constexpr bool cp = decltype(COPYC)::value;
+    auto hook = [&](int k) __attribute__((always_inline)) {
+      if (cp && k < PAIR_COPIES) load_part(k, j + 3, kd, vd);
+    };
+    auto kmax = [&](int kb) __attribute__((always_inline)) -> int {
+      int m = max(s[kb][0], s[kb][1]);
+#pragma unroll
+      for (int r = 2; r < 16; r += 2) m = max(max(m, s[kb][r]), s[kb][r + 1]);
+      return m;
+    };
+    auto load_kops = [&](int kb, v4i (&k)[4]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int dc = 0; dc < 4; ++dc) k[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
+    };
+    auto qk_kb = [&](int kb, const v4i (&k)[4]) __attribute__((always_inline)) {
+      v16i acc = {};
+#pragma unroll
+      for (int dc = 0; dc < 4; ++dc) acc = mfma_i8(k[dc], qop[dc], acc);
+      s[kb] = acc;
+    };
+    v8i pn[2];
+    float a8 = 0.f, bias = 0.f, a_s = 0.f, m_new = 0.f;
+    auto codes_kb = [&](int kb) __attribute__((always_inline)) {
+#pragma unroll
+      for (int d4 = 0; d4 < 4; ++d4) {
+        uint32_t w = 0;
+        if (PMODE == 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            w = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf((float)s[kb][4 * d4 + q], a8, bias), q, w);
+        } else {
+          float pe[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) pe[q] = __builtin_amdgcn_exp2f((float)s[kb][4 * d4 + q] * a_s - m_new) * 256.f;
+          w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(pe[0], pe[1], 0, false);
+          w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(pe[2], pe[3], (int)w, true);
+        }
+        int wi = (int)w;
+        pin(wi);  // formed in this region (pure values would otherwise be placed next to their use)
+        pn[kb >> 1][4 * (kb & 1) + d4] = wi;
+      }
+    };
+    // at most 32 registers of operands staged at any time
+    v8i va[2], vb[2];
+    v4i k0[4], k1[4];
+    // R0: value operands 0, 1
+    va[0] = load_vop(vt, 0);
+    va[1] = load_vop(vt, 1);
+    hook(0);
+    fence();
+    // R1: row sum and value products 0, 1; operands 2, 3; maxima of key blocks 0, 1
+    v4f rs = mfma_f8_16(ones16, pc[0], v4f{});
+    o[0] = mfma_f8(va[0], pc[0], o[0]);
+    o[1] = mfma_f8(va[1], pc[0], o[1]);
+    vb[0] = load_vop(vt, 2);
+    vb[1] = load_vop(vt, 3);
+    int mk0 = kmax(0), mk1 = kmax(1);
+    pin(mk0);
+    pin(mk1);
+    fence();
+    // R2: value products 2, 3; operands 4, 5; maxima of blocks 2, 3, m', alpha
+    o[2] = mfma_f8(vb[0], pc[0], o[2]);
+    o[3] = mfma_f8(vb[1], pc[0], o[3]);
+    va[0] = load_vop(vt, 4);
+    va[1] = load_vop(vt, 5);
+    a_s = (sq * ksc) * a.kappa;  // the oracle's order: fl(fl(s_q s_k) kappa)
+    int mx = max(max(mk0, mk1), max(kmax(2), kmax(3)));
+    mx = half_max(mx);
+    m_new = fmaxf(m_run, (float)mx * a_s);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    float alpha_p = alpha;
+    a8 = 8.f * a_s;
+    bias = a.cbias - 8.f * m_new;
+    pin(alpha_p);
+    pin(a8);
+    pin(bias);
+    pin(m_new);
+    hook(1);
+    fence();
+    // R3: row sum and value products 4, 5; operands 6, 7; key operands of block 0; codes of block 0
+    rs = mfma_f8_16(ones16, pc[1], rs);
+    o[0] = mfma_f8(va[0], pc[1], o[0]);
+    o[1] = mfma_f8(va[1], pc[1], o[1]);
+    vb[0] = load_vop(vt, 6);
+    vb[1] = load_vop(vt, 7);
+    codes_kb(0);
+    hook(2);
+    fence();
+    // R4: value products 6, 7, scores of block 0; key operands of block 1; codes of block 1
+    load_kops(0, k0);
+    o[2] = mfma_f8(vb[0], pc[1], o[2]);
+    o[3] = mfma_f8(vb[1], pc[1], o[3]);
+    qk_kb(0, k0);
+    codes_kb(1);
+    hook(3);
+    fence();
+    // R5: scores of block 1; key operands of block 2; codes of block 2
+    load_kops(1, k1);
+    qk_kb(1, k1);
+    load_kops(2, k0);
+    codes_kb(2);
+    hook(4);
+    fence();
+    // R6: scores of block 2; key operands of block 3; codes of block 3
+    qk_kb(2, k0);
+    load_kops(3, k1);
+    codes_kb(3);
+    fence();
+    // R7: scores of block 3
+    qk_kb(3, k1);
+    ksc = kscale[j + 2];
+    const float rsum = rs[0];
+    if (a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
+    rm_q[j & 7] = make_float2(rsum, m_run);
+    l_run += rsum;
+    if (tid < D) stash_mean(j, vt);
+    if (__builtin_amdgcn_ballot_w64(alpha_p != 1.f)) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha_p;
+      l_run *= alpha_p;
+    }
+    m_run = m_new;
+    pc[0] = pn[0];
+    pc[1] = pn[1];
+    end_iter(cp ? 2 : 0);
+  };
+
+  // prologue: K_0, K_1, pairs 0 and 1; scores of tile 0, its codes, scores of tile 1; pair 2
   const bool t2 = T > 1, t3 = T > 2;
-  __builtin_amdgcn_s_waitcnt(WAIT_VM0);  // the compiler's own loads have landed before any copy
-  load_k0();
-  load_pair(0, kb1, vb1);
-  if (t2) load_pair(1, kb2, vb2);
-  wait_pairs(t2 ? 2 : 1);  // K_0
+  wait_pairs(0);  // the compiler's own loads have landed before any copy
+  load_k(0, kb0);
+  if (t2) load_k(1, kb1);
+  load_pair(0, kb2, vb0);
+  if (t2) load_pair(1, kb3, vb1);
+  wait_pairs(t2 ? 2 : 1);  // K_0, K_1
   wg_barrier();
-  if (!lead) {
-    wait_pairs(t2 ? 1 : 0);  // pair 0
-    wg_barrier();
+  if (T == 1) qk(YES, 0, kb0);
+  else qk(NO, 0, kb0);
+  {
+    float alpha, m_new;
+    if (T == 1) softmax(YES, 0, pc, alpha, m_new);
+    else softmax(NO, 0, pc, alpha, m_new);
+    m_run = m_new;
   }
-  // M_{-1}: scores of tile 0; pair 2 copied
-  auto hook_m1 = [&](int k) __attribute__((always_inline)) {
-    if (t3) load_part(k, 2, kb3, vb3);
-  };
-  if (T == 1) mphase_m(NO, YES, YES, -1, kb0, vb0, hook_m1);
-  else mphase_m(NO, YES, NO, -1, kb0, vb0, hook_m1);
-  end_phase(lead ? (int)t2 + (int)t3 : -1);  // leaders: pair 0
-  // V_0
-  if (T == 1) vphase(YES, 0);
-  else vphase(NO, 0);
-  prefetch_v(vb1);
-  end_phase(lead ? -1 : (int)t3);  // followers: pair 1
+  if (t2) {
+    if (T == 2) qk(YES, 1, kb1);
+    else qk(NO, 1, kb1);
+  }
+  pin_state();
+  wg_barrier();  // every wave is done with K_0 before pair 2 overwrites it
+  if (t3) load_pair(2, kb0, vb2);
+  end_iter((int)t2 + (int)t3);  // pair 0
 
-  // steady-state tile step i (pair i+3 exists, i + 3 <= T - 1): M_i on the operands of V_i and
-  // K_{i+1} in buffer (ks) = (i+1) mod 4, copying pair i+3 into (kd, vd) = i mod 4; V_{i+1} (leaders
-  // stash mean i from vs) and the operands of V_{i+1} from vn = (i+2) mod 4
-  auto steady = [&](int i, uint8_t* kd, uint8_t* vd, const uint8_t* ks, const uint8_t* vs, const uint8_t* vn) __attribute__((always_inline)) {
-    auto hook = [&](int k) __attribute__((always_inline)) { load_part(k, i + 3, kd, vd); };
-    mphase_m(YES, YES, NO, i, ks, vs, hook);
-    end_phase(lead ? 2 : -1);  // leaders: pair i+1
-    if (lead) stash_mean(i, vs);
-    vphase(NO, i + 1);
-    prefetch_v(vn);
-    end_phase(lead ? -1 : 1);  // followers: pair i+2
-  };
-  int i = 0;
-  for (; i + 7 <= T; i += 4) {
-    steady(i, kb0, vb0, kb1, vb1, vb2);
-    steady(i + 1, kb1, vb1, kb2, vb2, vb3);
-    steady(i + 2, kb2, vb2, kb3, vb3, vb0);
-    steady(i + 3, kb3, vb3, kb0, vb0, vb1);
+  // steady state (pair j+3 exists), unrolled by four so every buffer is named statically:
+  // V_j in vb[j%4], K_{j+2} in kb[(j+2)%4], pair j+3 into (kb[(j+1)%4], vb[(j+3)%4])
+  int j = 0;
+  for (; j + 6 <= T - 1; j += 4) {  // the group's last iteration j + 3 still copies pair j + 6
+    iter_fast(YES, j, vb0, kb2, kb1, vb3);
+    iter_fast(YES, j + 1, vb1, kb3, kb2, vb0);
+    iter_fast(YES, j + 2, vb2, kb0, kb3, vb1);
+    iter_fast(YES, j + 3, vb3, kb1, kb0, vb2);
   }
-  if (i + 4 <= T) {
-    steady(i, kb0, vb0, kb1, vb1, vb2);
-    ++i;
-    if (i + 4 <= T) {
-      steady(i, kb1, vb1, kb2, vb2, vb3);
-      ++i;
-      if (i + 4 <= T) {
-        steady(i, kb2, vb2, kb3, vb3, vb0);
-        ++i;
+  if (j + 3 <= T - 1) {
+    iter_fast(YES, j, vb0, kb2, kb1, vb3);
+    ++j;
+    if (j + 3 <= T - 1) {
+      iter_fast(YES, j, vb1, kb3, kb2, vb0);
+      ++j;
+      if (j + 3 <= T - 1) {
+        iter_fast(YES, j, vb2, kb0, kb3, vb1);
+        ++j;
       }
     }
   }
-  // tail: no copies issued any more, every copy waited for
   auto kbuf = [&](int b) __attribute__((always_inline)) -> const uint8_t* {
     return b == 0 ? kb0 : (b == 1 ? kb1 : (b == 2 ? kb2 : kb3));
   };
   auto vbuf = [&](int b) __attribute__((always_inline)) -> const uint8_t* {
     return b == 0 ? vb0 : (b == 1 ? vb1 : (b == 2 ? vb2 : vb3));
   };
-  // tile steps T-3 (if it had no copy to issue), T-2 (scores and codes of the ragged last tile)
-  // and T-1 (its value product and the final means)
-  if (i == T - 3) {
-    const int b = (i + 1) & 3;
-    mphase_m(YES, YES, NO, i, kbuf(b), vbuf(b), nohook);
-    end_phase(0);
-    if (lead) stash_mean(i, vbuf(b));
-    vphase(NO, i + 1);
-    prefetch_v(vbuf((i + 2) & 3));
-    end_phase(0);
-    ++i;
+  // tail: iterations T-3 (scores of the last tile), T-2 (codes of the last tile), T-1
+  if (j == T - 3) {
+    iter(NO, YES, YES, YES, NO, j, vbuf(j & 3), kbuf((j + 2) & 3), kb0, vb0);
+    ++j;
   }
-  if (i == T - 2) {
-    const int b = (i + 1) & 3;
-    mphase_m(YES, YES, YES, i, kbuf(b), vbuf(b), nohook);
-    end_phase(0);
-    if (lead) stash_mean(i, vbuf(b));
-    vphase(YES, i + 1);
-    prefetch_v(vbuf((i + 2) & 3));
-    end_phase(0);
-    ++i;
+  if (j == T - 2) {
+    iter(NO, YES, NO, NO, YES, j, vbuf(j & 3), kb0, kb0, vb0);
+    ++j;
   }
-  {
-    const int b = T & 3;
-    mphase_m(YES, NO, NO, T - 1, kbuf(b), vbuf(b), nohook);
-    end_phase(0);
-    if (lead) stash_mean(T - 1, vbuf(b));
-    fold_rowsum(T - 1);
-    if (a.smooth_v) flush_means(((T - 1) >> 3) & 1, (T - 1) & 7);
-    end_phase(0);
-  }
-  if (lead) wg_barrier();
+  iter(NO, NO, NO, NO, NO, T - 1, vbuf((T - 1) & 3), kb0, kb0, vb0);
+  if (a.smooth_v) flush_means(((T - 1) >> 3) & 1, (T - 1) & 7);
 
   // epilogue: O = A s_V / l, bf16, row q written to token q_perm[q] (or q)
-  const int q = qt * FWD_QUERIES + wave * 32 + col;
+  const int q = qt * NQ + wave * 32 + col;
   if (q < a.N) {
     const float inv_l = 1.f / l_run;
     const int qo = a.q_perm ? clamp_index(a.q_perm[(size_t)bh * a.N + q], a.N) : q;
@@ -536,9 +617,9 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 }
 
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s) {
-  const dim3 grid((a.N + FWD_QUERIES - 1) / FWD_QUERIES, BH);
-  if (a.p_mode == 0) attn_fwd<0><<<grid, FWD_THREADS, 0, s>>>(a);
-  else attn_fwd<1><<<grid, FWD_THREADS, 0, s>>>(a);
+  const dim3 grid((a.N + NQ - 1) / NQ, BH);
+  if (a.p_mode == 0) attn_fwd<0><<<grid, NTH, 0, s>>>(a);
+  else attn_fwd<1><<<grid, NTH, 0, s>>>(a);
   return hipGetLastError();
 }
 
