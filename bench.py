@@ -12,7 +12,11 @@ reported in `attention` and, against the 8-bit matrix peak, in `roofline`; the p
 GB/s of algorithmic bytes in `prep`. `cpu_baseline` times the CPU oracle on a bounded sample of
 the same workload on the host cores (and the same sample gives the parity numbers).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+Beside the main line: `loop_slice`, the denoising-loop slice (8 calls of the same shape with
+interpolated inputs, grouping on calls 0 and 4) with prep GB/s, attention TOPS and the amortized
+grouping share; `large_layer`, the 75600-token 40-head layer timed stage by stage.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra]
 """
 from __future__ import annotations
 
@@ -98,12 +102,90 @@ def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=512):
                     oracle_rel_l2_vs_fp64=float(np.linalg.norm(o_ref - exact) / np.linalg.norm(exact))))
 
 
+def time_stages(fns, reps):
+    """Mean milliseconds of each callable in `fns`, run in sequence `reps` times on the current
+    stream, bracketed by HIP events."""
+    import torch
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(reps)]
+    torch.cuda.synchronize()
+    for e in ev:
+        e[0].record()
+        for i, f in enumerate(fns):
+            f()
+            e[i + 1].record()
+    torch.cuda.synchronize()
+    return [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(len(fns))]
+
+
+def loop_slice(vc, S, reps=3):
+    """Denoising-loop slice on the small-layer shape: 8 sequential calls with inputs interpolated
+    between two seeded fields, grouping recomputed on calls 0 (cold, 8 rounds) and 4 (warm-started
+    from call 0's centroids, 4 rounds), the permutation reused on the other calls."""
+    import torch
+    w = S.WORKLOADS[WORKLOAD]
+    B, H, N = w.B, w.H, w.N
+    steps = 8
+    calls = [S.make_interpolated(WORKLOAD, t, steps=steps) for t in range(steps)]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    calls = [tuple(dev(x) for x in c) for c in calls]
+    A = vc.Attention(B, H, w.grid)
+    O = torch.empty((B, H, N, 128), dtype=torch.int16, device="cuda")
+    cold, warm = vc.make_group_opts(k=32, iters=8), vc.make_group_opts(k=32, iters=4, warm_start=True)
+
+    def run_loop(record):
+        for t, (Q, K, V) in enumerate(calls):
+            stages = []
+            if t % 4 == 0:
+                A.gopts = cold if t == 0 else warm
+                stages.append(("group", lambda V=V: A.group(V)))
+            stages.append(("prep", lambda Q=Q, K=K, V=V: A.prep(Q, K, V)))
+            stages.append(("attn", lambda: A.forward(O)))
+            ms = time_stages([f for _, f in stages], 1)
+            for (name, _), m in zip(stages, ms):
+                record.setdefault(name, []).append(m)
+
+    run_loop({})  # warm-up
+    rec = {}
+    for _ in range(reps):
+        run_loop(rec)
+    ops = 4.0 * B * H * N * N * 128
+    t_group, t_prep, t_attn = (float(np.sum(rec[k])) / reps for k in ("group", "prep", "attn"))
+    return {"calls": steps, "regroup_every": 4, "loops_timed": reps,
+            "group_ms_per_loop": t_group, "prep_ms_per_loop": t_prep, "attn_ms_per_loop": t_attn,
+            "prep_gbs": prep_algorithmic_bytes(B, H, N) * steps / (t_prep * 1e-3) / 1e9,
+            "attention_tops": ops * steps / (t_attn * 1e-3) / 1e12,
+            "grouping_share": t_group / (t_group + t_prep + t_attn)}
+
+
+def large_layer(vc, S, reps=3):
+    """The large video-DiT layer (B=1, H=40, N=75600, 21x60x60 grid): grouping, preprocessing and
+    attention timed separately."""
+    import torch
+    w = S.WORKLOADS["dit_large"]
+    B, H, N = w.B, w.H, w.N
+    Q, K, V = (torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).cuda() for x in S.make_qkv("dit_large"))
+    A = vc.Attention(B, H, w.grid)
+    O = torch.empty((B, H, N, 128), dtype=torch.int16, device="cuda")
+    fns = [lambda: A.group(V), lambda: A.prep(Q, K, V), lambda: A.forward(O)]
+    time_stages(fns, 1)
+    t_group, t_prep, t_attn = time_stages(fns, reps)
+    ops = 4.0 * B * H * N * N * 128
+    tops = ops / (t_attn * 1e-3) / 1e12
+    return {"workload": f"B={B} H={H} N={N} (grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]}) d=128",
+            "group_ms": t_group, "prep_ms": t_prep, "attn_ms": t_attn, "attention_tops": tops,
+            "attention_frac_8bit_peak": tops / PEAK_8BIT_TOPS,
+            "prep_gbs": prep_algorithmic_bytes(B, H, N) / (t_prep * 1e-3) / 1e9,
+            "prep_frac_hbm": prep_algorithmic_bytes(B, H, N) / (t_prep * 1e-3) / 1e9 / PEAK_HBM_GBS}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the denoising-loop slice and the large layer (reported beside the main line)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -192,6 +274,11 @@ def main():
         "group": {"ms": t_group},
         "wall_s_timed": wall,
     }
+    if not args.no_extra:
+        print("[bench] denoising-loop slice", file=sys.stderr, flush=True)
+        out["loop_slice"] = loop_slice(vc, S)
+        print("[bench] large layer", file=sys.stderr, flush=True)
+        out["large_layer"] = large_layer(vc, S)
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle sample", file=sys.stderr, flush=True)
         O_host = S.bits_to_f32(O.cpu().numpy().view(np.uint16))
