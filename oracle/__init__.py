@@ -44,13 +44,17 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+QK_INT8, QK_MXFP4 = 0, 2
+
+
 class PrepCfg(C.Structure):
-    _fields_ = [(n, C.c_int32) for n in ("N", "F", "Ht", "Wd", "rope", "hadamard", "smooth_k", "smooth_v")]
+    _fields_ = [(n, C.c_int32) for n in ("N", "F", "Ht", "Wd", "rope", "hadamard", "smooth_k", "smooth_v",
+                                         "qk_fmt")]
 
 
 class AttnCfg(C.Structure):
     _fields_ = [("N", C.c_int32), ("hadamard", C.c_int32), ("smooth_v", C.c_int32), ("p_mode", C.c_int32),
-                ("sm_scale", C.c_float), ("beta", C.c_float)]
+                ("sm_scale", C.c_float), ("beta", C.c_float), ("qk_fmt", C.c_int32)]
 
 
 class GroupCfg(C.Structure):
@@ -73,6 +77,9 @@ def lib():
             _lib.or_expcast_code_u.argtypes = [C.c_float, C.c_float]
             _lib.or_expcast_code_acc.argtypes = [C.c_int32, C.c_float, C.c_float, C.c_float]
             _lib.or_exp_then_cast_code_acc.argtypes = [C.c_int32, C.c_float, C.c_float]
+            _lib.or_fp4_decode.restype = C.c_double
+            _lib.or_fp4_decode.argtypes = [C.c_uint8]
+            _lib.or_mx_score.restype = C.c_double
     return _lib
 
 
@@ -100,6 +107,37 @@ def e4m3_encode(x) -> np.ndarray:
     out = np.empty(x.shape, np.uint8)
     lib().or_e4m3_encode_array(C.c_int(x.size), _p(x), _p(out))
     return out
+
+
+def fp4_decode(c) -> np.ndarray:
+    """E2M1 (OCP MX FP4) codes 0..15 to values."""
+    c = np.asarray(c, np.uint8)
+    return np.vectorize(lambda v: lib().or_fp4_decode(int(v)), otypes=[np.float64])(c) if c.size else np.zeros(c.shape)
+
+
+def fp4_encode(x) -> np.ndarray:
+    x = _c(x, np.float32)
+    out = np.empty(x.shape, np.uint8)
+    lib().or_fp4_encode_array(C.c_int(x.size), _p(x), _p(out))
+    return out
+
+
+def mx_blocks(x):
+    """MXFP4 quantization of fp32 data [..., 32k] by blocks of 32: (codes uint8 [...], scale bytes)."""
+    x = _c(x, np.float32)
+    assert x.shape[-1] % 32 == 0
+    nb = x.size // 32
+    codes = np.empty(x.shape, np.uint8)
+    scales = np.empty(x.shape[:-1] + (x.shape[-1] // 32,), np.uint8)
+    lib().or_mx_blocks(C.c_int(nb), _p(x), _p(codes), _p(scales))
+    return codes, scales
+
+
+def mx_score(q, qs, k, ks) -> float:
+    """Exact score of one query row and one key row from their MX codes [128] and scales [4]."""
+    q, k = _c(q, np.uint8), _c(k, np.uint8)
+    qs, ks = _c(qs, np.uint8), _c(ks, np.uint8)
+    return float(lib().or_mx_score(_p(q), _p(qs), _p(k), _p(ks)))
 
 
 def bf16_round(x) -> np.ndarray:
@@ -159,10 +197,13 @@ def rope_apply(x, grid) -> np.ndarray:
 # preprocessing, attention, grouping
 # ---------------------------------------------------------------------------------------------
 
-def prep(Q, K, V, grid, perm=None, q_perm=None, rope=True, hadamard=True, smooth_k=True, smooth_v=True):
+def prep(Q, K, V, grid, perm=None, q_perm=None, rope=True, hadamard=True, smooth_k=True, smooth_v=True,
+         qk_fmt=QK_INT8):
     """Q, K, V: uint16 bf16 bits [B, H, N, 128]. perm / q_perm: int32 [B, H, N] or None.
 
-    Returns a dict of numpy arrays (see ``or_prep_head`` in vc_oracle.c for the layouts).
+    Returns a dict of numpy arrays (see ``or_prep_head`` in vc_oracle.c for the layouts); with
+    qk_fmt = QK_MXFP4 also q_mx / k_mx (one E2M1 code per byte [B, H, Np, 128]) and q_mxs / k_mxs
+    (E8M0 scale bytes [B, H, Np, 4]).
     """
     Q, K, V = (_c(t, np.uint16) for t in (Q, K, V))
     B, H, N, d = Q.shape
@@ -181,14 +222,19 @@ def prep(Q, K, V, grid, perm=None, q_perm=None, rope=True, hadamard=True, smooth
         v=np.zeros((B, H, Np, D), np.uint8), v_scale=np.zeros((B, H, D), np.float32),
         v_mean=np.zeros((B, H, T, D), np.uint16),
     )
-    cfg = PrepCfg(N, F, Ht, Wd, int(rope), int(hadamard), int(smooth_k), int(smooth_v))
+    mx = qk_fmt == QK_MXFP4
+    if mx:
+        out.update(q_mx=np.zeros((B, H, Np, D), np.uint8), q_mxs=np.zeros((B, H, Np, 4), np.uint8),
+                   k_mx=np.zeros((B, H, Np, D), np.uint8), k_mxs=np.zeros((B, H, Np, 4), np.uint8))
+    cfg = PrepCfg(N, F, Ht, Wd, int(rope), int(hadamard), int(smooth_k), int(smooth_v), int(qk_fmt))
     rc = lib().or_prep(C.c_int(B * H), C.byref(cfg), _p(Q), _p(K), _p(V), _p(perm), _p(q_perm),
                        _p(cos_t), _p(sin_t), _p(out["q"]), _p(out["q_scale"]), _p(out["k"]),
                        _p(out["k_scale"]), _p(out["k_mean"]), _p(out["v"]), _p(out["v_scale"]),
-                       _p(out["v_mean"]))
+                       _p(out["v_mean"]), _p(out.get("q_mx")), _p(out.get("q_mxs")), _p(out.get("k_mx")),
+                       _p(out.get("k_mxs")))
     if rc != 0:
         raise MemoryError("oracle prep failed")
-    out.update(N=N, grid=(F, Ht, Wd), hadamard=bool(hadamard), smooth_v=bool(smooth_v))
+    out.update(N=N, grid=(F, Ht, Wd), hadamard=bool(hadamard), smooth_v=bool(smooth_v), qk_fmt=int(qk_fmt))
     return out
 
 
@@ -205,17 +251,23 @@ def attention(pp, rows, bh=None, p_mode=P_EXPCAST, sm_scale=None, beta=-0.35):
     rows = _c(rows, np.int32)
     bh = list(range(B * H)) if bh is None else list(bh)
     out = np.zeros((len(bh), rows.size, D), np.float64)
-    cfg = AttnCfg(N, int(pp["hadamard"]), int(pp["smooth_v"]), int(p_mode), float(sm_scale), float(beta))
+    qk_fmt = int(pp.get("qk_fmt", QK_INT8))
+    cfg = AttnCfg(N, int(pp["hadamard"]), int(pp["smooth_v"]), int(p_mode), float(sm_scale), float(beta), qk_fmt)
     q = pp["q"].reshape(B * H, -1, D); qs = pp["q_scale"].reshape(B * H, -1)
     k = pp["k"].reshape(B * H, -1, D); ks = pp["k_scale"].reshape(B * H, -1)
     v = pp["v"].reshape(B * H, -1, D); vs = pp["v_scale"].reshape(B * H, D)
     vm = pp["v_mean"].reshape(B * H, -1, D)
+    mx = qk_fmt == QK_MXFP4
+    if mx:
+        qm = pp["q_mx"].reshape(B * H, -1, D); qms = pp["q_mxs"].reshape(B * H, -1, 4)
+        km = pp["k_mx"].reshape(B * H, -1, D); kms = pp["k_mxs"].reshape(B * H, -1, 4)
     for t, h in enumerate(bh):
         o = np.zeros((rows.size, D), np.float64)
+        mxargs = [_p(_c(a[h], np.uint8)) for a in (qm, qms, km, kms)] if mx else [None] * 4
         lib().or_attn_head(C.byref(cfg), _p(_c(q[h], np.int8)), _p(_c(qs[h], np.float32)),
                            _p(_c(k[h], np.int8)), _p(_c(ks[h], np.float32)), _p(_c(v[h], np.uint8)),
                            _p(_c(vs[h], np.float32)), _p(_c(vm[h], np.uint16)), C.c_int(rows.size),
-                           _p(rows), _p(o))
+                           _p(rows), _p(o), *mxargs)
         out[t] = o
     return out
 

@@ -112,30 +112,39 @@ int or_expcast_code_u(float u, float beta)
     return (int)r;
 }
 
-/* The same map inside the attention loop. The score of an int32 dot product acc is
- * t = acc * a in log2 units (a folds the two block scales, 1/sqrt(d), log2(e) and, with the
- * Hadamard rotation, 1/128). With running maximum m', u = t - m', so
- * 8(u+8)+56+beta = 8a*acc + (120 + beta - 8m'): one fused multiply-add in fp32.
- * READING: the multiply-add is fmaf(acc, 8a, fl(fl(120+beta) - 8m')); 8a and 8m' are exact. */
-int or_expcast_code_acc(int32_t acc, float a, float m_new, float beta)
+/* The same map inside the attention loop. The score s of a query and a key (the int32 dot
+ * product of the INT8 codes, or the fp32 score of the MXFP4 product) times a is in log2 units (a
+ * folds the block scales, 1/sqrt(d), log2(e) and, with the Hadamard rotation, 1/128). With
+ * running maximum m', u = s a - m', so 8(u+8)+56+beta = 8a*s + (120 + beta - 8m'): one fused
+ * multiply-add in fp32.
+ * READING: the multiply-add is fmaf(s, 8a, fl(fl(120+beta) - 8m')); 8a and 8m' are exact. */
+int or_expcast_code_s(float s, float a, float m_new, float beta)
 {
     float cst = 120.0f + beta;
     float bias = cst - 8.0f * m_new;
-    float c = fmaf((float)acc, 8.0f * a, bias);
+    float c = fmaf(s, 8.0f * a, bias);
     float r = rintf(c);
     if (r < 0.0f) r = 0.0f;
     if (r > 120.0f) r = 120.0f;
     return (int)r;
 }
+int or_expcast_code_acc(int32_t acc, float a, float m_new, float beta)
+{
+    return or_expcast_code_s((float)acc, a, m_new, beta);  /* |acc| < 2^24: exact */
+}
 
 /* The conventional path the paper compares against: exponentiate in fp32, scale by 2^8, cast
  * to E4M3 (Sec. 3.3, first listing). exp2 is evaluated in fp64 and rounded once to fp32. */
-int or_exp_then_cast_code_acc(int32_t acc, float a, float m_new)
+int or_exp_then_cast_code_s(float s, float a, float m_new)
 {
-    float t = (float)acc * a;
+    float t = s * a;
     float u = t - m_new;
     float p = (float)exp2((double)u);
     return (int)or_e4m3_encode(p * 256.0f);
+}
+int or_exp_then_cast_code_acc(int32_t acc, float a, float m_new)
+{
+    return or_exp_then_cast_code_s((float)acc, a, m_new);
 }
 
 /* ------------------------------------------------------------------------------------------ */
@@ -243,12 +252,92 @@ static void quant_block_i8(const float *x, int valid, int8_t *codes, float *scal
 }
 
 /* ------------------------------------------------------------------------------------------ */
+/* MXFP4 quantizer for Q and K (the 4-bit variant: OCP microscaling, 32-element blocks)        */
+/* ------------------------------------------------------------------------------------------ */
+
+/* FP4 E2M1 element of the OCP MX formats: sign bit 3, exponent field bits 2..1 (bias 1),
+ * mantissa bit 0. Exponent field 0 encodes the subnormal m/2, otherwise 2^(e-1) (1 + m/2):
+ * magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6. No infinities or NaN. */
+double or_fp4_decode(uint8_t c)
+{
+    const int s = (c >> 3) & 1, e = (c >> 1) & 3, m = c & 1;
+    const double mag = e == 0 ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);
+    return s ? -mag : mag;
+}
+
+/* Nearest E2M1 value, ties to the code with mantissa bit 0, saturating at magnitude 6.
+ * READING: a value whose magnitude rounds to 0 gets the code +0 (0x0). The search runs over the
+ * 8 magnitudes in increasing order. */
+uint8_t or_fp4_encode(float x)
+{
+    const double a = fabs((double)x);
+    int best = 0;
+    double bd = fabs(a - or_fp4_decode(0));
+    for (int c = 1; c < 8; ++c) {
+        const double d = fabs(a - or_fp4_decode((uint8_t)c));
+        if (d < bd || (d == bd && (c & 1) == 0)) { bd = d; best = c; }
+    }
+    if (a > 6.0) best = 7;
+    return (uint8_t)(best == 0 ? 0 : ((x < 0.0f ? 8 : 0) | best));
+}
+
+/* One block of 32 consecutive channels of a row. READING (OCP MX shared-scale rule): with amax
+ * the block's largest magnitude, the shared exponent is X = floor(log2(amax)) - 2 (2 is the
+ * largest E2M1 exponent), clamped to [-127, 127], stored as the E8M0 byte X + 127; each element
+ * is or_fp4_encode(x * 2^-X) (the scaling is exact). An all-zero block gets the byte 127 and
+ * zero codes. */
+void or_mx_block(const float *x, uint8_t *codes, uint8_t *scale)
+{
+    float amax = 0.0f;
+    for (int c = 0; c < 32; ++c)
+        if (fabsf(x[c]) > amax) amax = fabsf(x[c]);
+    if (amax == 0.0f) {
+        *scale = 127;
+        memset(codes, 0, 32);
+        return;
+    }
+    int E;
+    frexpf(amax, &E);  /* amax = f 2^E, f in [0.5, 1): floor(log2(amax)) = E - 1 */
+    int X = E - 1 - 2;
+    if (X < -127) X = -127;
+    if (X > 127) X = 127;
+    *scale = (uint8_t)(X + 127);
+    for (int c = 0; c < 32; ++c) codes[c] = or_fp4_encode(ldexpf(x[c], -X));
+}
+
+/* Rows of a 128-row block: four MX blocks per valid row; padded rows get zero codes and the
+ * scale byte 127. codes: one E2M1 code per byte [128 x 128]; scales [128 x 4]. */
+static void quant_block_mx(const float *x, int valid, uint8_t *codes, uint8_t *scales)
+{
+    memset(codes, 0, (size_t)BLK * D);
+    memset(scales, 127, (size_t)BLK * 4);
+    for (int r = 0; r < valid; ++r)
+        for (int b = 0; b < 4; ++b) or_mx_block(&x[r * D + 32 * b], &codes[r * D + 32 * b], &scales[r * 4 + b]);
+}
+
+/* The score of one query row against one key row from their MX codes, exact (fp64):
+ * sum over the four blocks of 2^(Xq + Xk) times the block's dot product of the decoded elements. */
+double or_mx_score(const uint8_t *q, const uint8_t *qs, const uint8_t *k, const uint8_t *ks)
+{
+    double s = 0.0;
+    for (int b = 0; b < 4; ++b) {
+        double dot = 0.0;
+        for (int c = 32 * b; c < 32 * b + 32; ++c) dot += or_fp4_decode(q[c]) * or_fp4_decode(k[c]);
+        s += ldexp(dot, ((int)qs[b] - 127) + ((int)ks[b] - 127));
+    }
+    return s;
+}
+
+/* ------------------------------------------------------------------------------------------ */
 /* Preprocessing of one (batch, head): Q, K, V -> codes, scales, means (Sec. 3.4, App. B)     */
 /* ------------------------------------------------------------------------------------------ */
+
+enum { OR_QK_INT8 = 0, OR_QK_MXFP4 = 2 };
 
 typedef struct {
     int32_t N, F, Ht, Wd;
     int32_t rope, hadamard, smooth_k, smooth_v;
+    int32_t qk_fmt;  /* OR_QK_INT8 or OR_QK_MXFP4 */
 } or_prep_cfg;
 
 /* Inputs: Q, K, V as bf16 bit patterns [N x 128] in token order; perm (K/V gather, NULL =
@@ -259,12 +348,17 @@ typedef struct {
  *   k_mean  fp32 [128]                            (zeros when smooth_k = 0)
  *   v_codes E4M3 bytes [Np x 128], v_scale [128]  (permuted order, residual after demeaning)
  *   v_mean  bf16 bits [T x 128]                   (zeros when smooth_v = 0)
+ * With qk_fmt = OR_QK_MXFP4 the Q and K rows are quantized by MX blocks instead (the INT8
+ * outputs are not written): q_mx, k_mx one E2M1 code per byte [Np x 128], q_mxs, k_mxs E8M0
+ * scale bytes [Np x 4].
  * Returns 0, or -1 on allocation failure. */
 int or_prep_head(const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, const uint16_t *V,
                  const int32_t *perm, const int32_t *q_perm, const float *cos_t, const float *sin_t,
                  int8_t *q_codes, float *q_scale, int8_t *k_codes, float *k_scale, float *k_mean,
-                 uint8_t *v_codes, float *v_scale, uint16_t *v_mean)
+                 uint8_t *v_codes, float *v_scale, uint16_t *v_mean,
+                 uint8_t *q_mx, uint8_t *q_mxs, uint8_t *k_mx, uint8_t *k_mxs)
 {
+    const int mx = cfg->qk_fmt == OR_QK_MXFP4;
     const int N = cfg->N, T = (N + BLK - 1) / BLK, Np = T * BLK;
     float *xq = calloc((size_t)Np * D, sizeof(float));
     float *kr = calloc((size_t)N * D, sizeof(float));
@@ -282,7 +376,10 @@ int or_prep_head(const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, c
     }
     for (int j = 0; j < T; ++j) {
         int valid = N - j * BLK < BLK ? N - j * BLK : BLK;
-        quant_block_i8(&xq[(size_t)j * BLK * D], valid, &q_codes[(size_t)j * BLK * D], &q_scale[j]);
+        if (mx)
+            quant_block_mx(&xq[(size_t)j * BLK * D], valid, &q_mx[(size_t)j * BLK * D], &q_mxs[(size_t)j * BLK * 4]);
+        else
+            quant_block_i8(&xq[(size_t)j * BLK * D], valid, &q_codes[(size_t)j * BLK * D], &q_scale[j]);
     }
 
     /* K: RoPE in token order. */
@@ -318,7 +415,10 @@ int or_prep_head(const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, c
     }
     for (int j = 0; j < T; ++j) {
         int valid = N - j * BLK < BLK ? N - j * BLK : BLK;
-        quant_block_i8(&xk[(size_t)j * BLK * D], valid, &k_codes[(size_t)j * BLK * D], &k_scale[j]);
+        if (mx)
+            quant_block_mx(&xk[(size_t)j * BLK * D], valid, &k_mx[(size_t)j * BLK * D], &k_mxs[(size_t)j * BLK * 4]);
+        else
+            quant_block_i8(&xk[(size_t)j * BLK * D], valid, &k_codes[(size_t)j * BLK * D], &k_scale[j]);
     }
 
     /* V' = V[perm]; block means and residuals (eq. block-demeaning). */
@@ -375,6 +475,7 @@ enum { OR_P_EXPCAST = 0, OR_P_EXP_THEN_CAST = 1 };
 typedef struct {
     int32_t N, hadamard, smooth_v, p_mode;
     float sm_scale, beta;
+    int32_t qk_fmt;  /* OR_QK_INT8 or OR_QK_MXFP4 */
 } or_attn_cfg;
 
 /* Score scale in log2 units for one (query block, key block) pair:
@@ -396,36 +497,48 @@ static float score_kappa(const or_attn_cfg *cfg)
  * (App. B), so one final multiply by s_V returns value units. */
 static void attn_row(const or_attn_cfg *cfg, int i, const int8_t *qc, const float *qs,
                      const int8_t *kc, const float *ks, const uint8_t *vc, const float *vs,
-                     const uint16_t *vm, double *out)
+                     const uint16_t *vm, const uint8_t *qm, const uint8_t *qms, const uint8_t *km,
+                     const uint8_t *kms, double *out)
 {
     const int N = cfg->N, T = (N + BLK - 1) / BLK;
+    const int mx = cfg->qk_fmt == OR_QK_MXFP4;
     const float kappa = score_kappa(cfg);
-    const float sq = qs[i / BLK];
+    const float sq = mx ? 1.0f : qs[i / BLK];
     const int8_t *q = &qc[(size_t)i * D];
     double A[D], pv[D], mu_code[D];
     double l = 0.0;
     float m = -INFINITY;
-    int32_t acc[BLK];
+    float sc[BLK];
     for (int c = 0; c < D; ++c) A[c] = 0.0;
     for (int j = 0; j < T; ++j) {
         const int valid = N - j * BLK < BLK ? N - j * BLK : BLK;
-        const float a = (sq * ks[j]) * kappa;
-        int32_t M = INT32_MIN;
+        /* INT8: s = the exact int32 dot product of the codes, a = fl(fl(s_q s_k) kappa);
+         * MXFP4 (READING): s = the exact score of the MX codes rounded once to fp32 (the block
+         * scales are inside s), a = kappa. */
+        const float a = mx ? kappa : (sq * ks[j]) * kappa;
+        float M = -INFINITY;
         for (int s = 0; s < valid; ++s) {
-            const int8_t *k = &kc[(size_t)(j * BLK + s) * D];
-            int32_t dot = 0;
-            for (int c = 0; c < D; ++c) dot += (int32_t)q[c] * (int32_t)k[c];
-            acc[s] = dot;
-            if (dot > M) M = dot;
+            const size_t key = (size_t)(j * BLK + s);
+            float v;
+            if (mx) {
+                v = (float)or_mx_score(&qm[(size_t)i * D], &qms[(size_t)i * 4], &km[key * D], &kms[key * 4]);
+            } else {
+                const int8_t *k = &kc[key * D];
+                int32_t dot = 0;
+                for (int c = 0; c < D; ++c) dot += (int32_t)q[c] * (int32_t)k[c];
+                v = (float)dot;  /* |dot| <= 128 * 127^2 < 2^24: exact */
+            }
+            sc[s] = v;
+            if (v > M) M = v;
         }
-        float tmax = (float)M * a;
+        float tmax = M * a;
         float m_new = m > tmax ? m : tmax;
         double alpha = (m == -INFINITY) ? 0.0 : exp2((double)m - (double)m_new);
         double r = 0.0;
         for (int c = 0; c < D; ++c) pv[c] = 0.0;
         for (int s = 0; s < valid; ++s) {
-            int code = cfg->p_mode == OR_P_EXPCAST ? or_expcast_code_acc(acc[s], a, m_new, cfg->beta)
-                                                   : or_exp_then_cast_code_acc(acc[s], a, m_new);
+            int code = cfg->p_mode == OR_P_EXPCAST ? or_expcast_code_s(sc[s], a, m_new, cfg->beta)
+                                                   : or_exp_then_cast_code_s(sc[s], a, m_new);
             double p = or_e4m3_decode((uint8_t)code);
             if (p == 0.0) continue;
             r += p;
@@ -446,12 +559,13 @@ static void attn_row(const or_attn_cfg *cfg, int i, const int8_t *qc, const floa
 void or_attn_head(const or_attn_cfg *cfg, const int8_t *q_codes, const float *q_scale,
                   const int8_t *k_codes, const float *k_scale, const uint8_t *v_codes,
                   const float *v_scale, const uint16_t *v_mean, int n_rows, const int32_t *rows,
-                  double *out)
+                  double *out, const uint8_t *q_mx, const uint8_t *q_mxs, const uint8_t *k_mx,
+                  const uint8_t *k_mxs)
 {
 #pragma omp parallel for schedule(dynamic, 1)
     for (int t = 0; t < n_rows; ++t)
         attn_row(cfg, rows[t], q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, v_mean,
-                 &out[(size_t)t * D]);
+                 q_mx, q_mxs, k_mx, k_mxs, &out[(size_t)t * D]);
 }
 
 /* The same online recurrence on full-precision operands (no quantizer, exact exponential):
@@ -734,16 +848,20 @@ void or_group_codes(int N, const uint16_t *V, int8_t *x, float *scale_out)
 int or_prep(int BH, const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, const uint16_t *V,
             const int32_t *perm, const int32_t *q_perm, const float *cos_t, const float *sin_t,
             int8_t *q_codes, float *q_scale, int8_t *k_codes, float *k_scale, float *k_mean,
-            uint8_t *v_codes, float *v_scale, uint16_t *v_mean)
+            uint8_t *v_codes, float *v_scale, uint16_t *v_mean,
+            uint8_t *q_mx, uint8_t *q_mxs, uint8_t *k_mx, uint8_t *k_mxs)
 {
     const size_t N = (size_t)cfg->N, T = (N + BLK - 1) / BLK, Np = T * BLK;
+    const int mx = cfg->qk_fmt == OR_QK_MXFP4;
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
     for (int h = 0; h < BH; ++h) {
         int rc = or_prep_head(cfg, Q + h * N * D, K + h * N * D, V + h * N * D,
                               perm ? perm + h * N : NULL, q_perm ? q_perm + h * N : NULL, cos_t, sin_t,
                               q_codes + h * Np * D, q_scale + h * T, k_codes + h * Np * D, k_scale + h * T,
-                              k_mean + h * D, v_codes + h * Np * D, v_scale + h * D, v_mean + h * T * D);
+                              k_mean + h * D, v_codes + h * Np * D, v_scale + h * D, v_mean + h * T * D,
+                              mx ? q_mx + h * Np * D : NULL, mx ? q_mxs + h * Np * 4 : NULL,
+                              mx ? k_mx + h * Np * D : NULL, mx ? k_mxs + h * Np * 4 : NULL);
         bad |= (rc != 0);
     }
     return bad ? -1 : 0;
@@ -768,6 +886,14 @@ int or_group(int BH, const or_group_cfg *cfg, const uint16_t *V, const float *ce
 void or_e4m3_encode_array(int n, const float *x, uint8_t *out)
 {
     for (int i = 0; i < n; ++i) out[i] = or_e4m3_encode(x[i]);
+}
+void or_fp4_encode_array(int n, const float *x, uint8_t *out)
+{
+    for (int i = 0; i < n; ++i) out[i] = or_fp4_encode(x[i]);
+}
+void or_mx_blocks(int n_blocks, const float *x, uint8_t *codes, uint8_t *scales)
+{
+    for (int b = 0; b < n_blocks; ++b) or_mx_block(&x[32 * b], &codes[32 * b], &scales[b]);
 }
 void or_e4m3_decode_array(int n, const uint8_t *b, double *out)
 {
