@@ -60,11 +60,16 @@ typedef struct {
     int32_t F, Ht, Wd;      /* latent grid: frames, rows, cols */
 } vc_shape;
 
-enum { VC_QK_INT8 = 0 };                          /* per-128-row-block symmetric INT8 Q and K */
+enum { VC_QK_INT8 = 0,      /* per-128-row-block symmetric INT8 Q and K */
+       VC_QK_MXFP4 = 2 };   /* OCP MX FP4 (E2M1) Q and K, one E8M0 scale per 32 channels of a row */
 enum { VC_P_EXPCAST = 0, VC_P_EXP_THEN_CAST = 1 };
 
 /* Options of the low-bit path.
- *   qk_fmt   : VC_QK_INT8 (the only value accepted).
+ *   qk_fmt   : VC_QK_INT8 (the method's 8-bit path) or VC_QK_MXFP4 (the 4-bit variant: Q and K
+ *              quantized after the Hadamard rotation by 32-channel blocks, shared exponent
+ *              floor(log2(amax)) - 2, elements rounded to the nearest E2M1 value with ties to the
+ *              even code and saturation at 6; the scores come out of the scaled FP4 matrix
+ *              product in fp32; P and V stay 8-bit).
  *   p_mode   : VC_P_EXPCAST (ExpCast-FP8, eq. direct-fp8) or VC_P_EXP_THEN_CAST (fp32 exp2,
  *              scale by 2^8, E4M3 round-to-nearest-even cast: the conventional path).
  *   rope     : 1 = apply the 3-axis rotary embedding in the preprocessing (pairs 0..21 turn with
@@ -112,6 +117,16 @@ typedef struct {
  *          ((rb*4 + dc)*2 + dh)*512 + r*16 + e. q rows are in query order (q_perm order when a
  *          q_perm is given); k rows in permuted order K' = K[perm]. Padded rows hold 0.
  *   q_scale, k_scale : fp32 [B, H, T], one scale per 128-row block (code * scale = value).
+ *   With qk_fmt = VC_QK_MXFP4 instead:
+ *   q, k : packed E2M1 codes, B*H*Np*64 bytes. Per (b, h) and 128-row block j, the 8192 bytes are
+ *          ordered [rb 4][m 2][h 2][r 32][16 bytes]: channel ch of row `row` is the nibble
+ *          ch % 2 (0 = low) of byte ((rb*2 + m)*2 + h)*512 + r*16 + (ch % 32)/2 with rb = row/32,
+ *          r = row%32, m = ch/64, h = (ch%64)/32 (lane h*32 + r of the scaled matrix product
+ *          holds one 32-channel block of one row). Padded rows hold 0.
+ *   q_mx_scale, k_mx_scale : E8M0 bytes (value 2^(byte - 127)), B*H*Np*4 bytes. Per (b, h) and
+ *          block j, the 512 bytes are ordered [lane 64][rb 4][m 2]: the scale of row 32*rb + r,
+ *          channels 64*m + 32*h .. + 31 sits at (h*32 + r)*8 + rb*2 + m. Padded rows hold 127.
+ *   q_scale, k_scale are not used.
  *   k_mean : fp32 [B, H, 128], the key channel mean subtracted before quantizing (0 if off).
  *   v    : E4M3 (OCP e4m3fn) bytes of the demeaned residual, B*H*Np*128 bytes, permuted order.
  *          Per (b, h) and 128-row block, ordered [kc 2][db 4][kh 2][sh 2][c 32][t 16]: with
@@ -131,6 +146,8 @@ typedef struct {
     uint8_t *v;
     float *v_scale;
     uint16_t *v_mean;
+    uint8_t *q_mx_scale;   /* VC_QK_MXFP4 only (may be NULL otherwise) */
+    uint8_t *k_mx_scale;
 } vc_prepped;
 
 /* Fill *o with the method's defaults: INT8 QK, ExpCast-FP8, RoPE, Hadamard, key centering and

@@ -21,6 +21,7 @@ VC_OK = 0
 STATUS = {0: "VC_OK", 1: "VC_ERR_NULL", 2: "VC_ERR_SHAPE", 3: "VC_ERR_UNSUPPORTED", 4: "VC_ERR_WORKSPACE",
           5: "VC_ERR_ALIGN", 6: "VC_ERR_HIP", 7: "VC_ERR_INTERNAL"}
 P_EXPCAST, P_EXP_THEN_CAST = 0, 1
+QK_INT8, QK_MXFP4 = 0, 2
 GROUP_IDENTITY, GROUP_CUBE, GROUP_KMEANS = 0, 1, 2
 
 
@@ -50,7 +51,8 @@ class GroupOpts(C.Structure):
 
 
 class Prepped(C.Structure):
-    _fields_ = [(n, C.c_void_p) for n in ("q", "q_scale", "k", "k_scale", "k_mean", "v", "v_scale", "v_mean")]
+    _fields_ = [(n, C.c_void_p) for n in ("q", "q_scale", "k", "k_scale", "k_mean", "v", "v_scale", "v_mean",
+                                          "q_mx_scale", "k_mx_scale")]
 
 
 _lib = None
@@ -98,9 +100,10 @@ def make_shape(B: int, H: int, grid) -> Shape:
 
 
 def make_opts(p_mode=P_EXPCAST, rope=True, hadamard=True, smooth_k=True, smooth_v=True, sm_scale=0.0,
-              beta=-0.35) -> Opts:
+              beta=-0.35, qk_fmt=QK_INT8) -> Opts:
     o = Opts()
     lib().vc_opts_default(C.byref(o))
+    o.qk_fmt = int(qk_fmt)
     o.p_mode, o.rope, o.hadamard = int(p_mode), int(rope), int(hadamard)
     o.smooth_k, o.smooth_v, o.sm_scale, o.beta = int(smooth_k), int(smooth_v), float(sm_scale), float(beta)
     return o
@@ -148,24 +151,33 @@ class PreppedBuffers:
     v: object
     v_scale: object
     v_mean: object
+    q_mx_scale: object = None
+    k_mx_scale: object = None
 
     def as_struct(self) -> Prepped:
-        return Prepped(*(t.data_ptr() for t in (self.q, self.q_scale, self.k, self.k_scale, self.k_mean,
-                                                  self.v, self.v_scale, self.v_mean)))
+        return Prepped(*(None if t is None else t.data_ptr()
+                         for t in (self.q, self.q_scale, self.k, self.k_scale, self.k_mean, self.v, self.v_scale,
+                                   self.v_mean, self.q_mx_scale, self.k_mx_scale)))
 
 
-def alloc_prepped(shape: Shape, device="cuda") -> PreppedBuffers:
+def alloc_prepped(shape: Shape, device="cuda", qk_fmt: int = None) -> PreppedBuffers:
+    """Buffers for vc_attn_prep / vc_attn_forward. INT8: q, k int8 [B, H, Np, 128] and fp32 block
+    scales; MXFP4: q, k packed codes [B, H, Np, 64] bytes and E8M0 scale bytes [B, H, Np, 4]."""
     import torch
     B, H, N = shape.B, shape.H, shape.N
     T = (N + 127) // 128
     Np = 128 * T
     e = dict(device=device)
+    mx = qk_fmt == QK_MXFP4
+    cw = D // 2 if mx else D
     return PreppedBuffers(
-        q=torch.empty((B, H, Np, D), dtype=torch.int8, **e), q_scale=torch.empty((B, H, T), dtype=torch.float32, **e),
-        k=torch.empty((B, H, Np, D), dtype=torch.int8, **e), k_scale=torch.empty((B, H, T), dtype=torch.float32, **e),
+        q=torch.empty((B, H, Np, cw), dtype=torch.int8, **e), q_scale=torch.empty((B, H, T), dtype=torch.float32, **e),
+        k=torch.empty((B, H, Np, cw), dtype=torch.int8, **e), k_scale=torch.empty((B, H, T), dtype=torch.float32, **e),
         k_mean=torch.empty((B, H, D), dtype=torch.float32, **e),
         v=torch.empty((B, H, Np, D), dtype=torch.uint8, **e), v_scale=torch.empty((B, H, D), dtype=torch.float32, **e),
-        v_mean=torch.empty((B, H, T, D), dtype=torch.int16, **e))
+        v_mean=torch.empty((B, H, T, D), dtype=torch.int16, **e),
+        q_mx_scale=torch.empty((B, H, Np, 4), dtype=torch.uint8, **e) if mx else None,
+        k_mx_scale=torch.empty((B, H, Np, 4), dtype=torch.uint8, **e) if mx else None)
 
 
 def vc_attn_group(shape, gopts, V, centroids, labels, perm, inv_perm, ws, stream=None):
@@ -212,7 +224,7 @@ class Attention:
         self.inv_perm = torch.empty((B, H, N), **e)
         self.labels = torch.empty((B, H, N), **e)
         self.centroids = torch.zeros((B, H, max(self.gopts.k, 1), D), dtype=torch.float32, device=device)
-        self.prepped = alloc_prepped(self.shape, device)
+        self.prepped = alloc_prepped(self.shape, device, self.opts.qk_fmt)
         cos_t, sin_t = rope_tables_host(*grid)
         self.rope_cos = torch.from_numpy(cos_t).to(device)
         self.rope_sin = torch.from_numpy(sin_t).to(device)

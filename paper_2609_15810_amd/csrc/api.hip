@@ -29,7 +29,7 @@ vc_status check_shape(const vc_shape* s) {
 
 vc_status check_opts(const vc_opts* o) {
   if (!o) return VC_ERR_NULL;
-  if (o->qk_fmt != VC_QK_INT8) return VC_ERR_UNSUPPORTED;
+  if (o->qk_fmt != VC_QK_INT8 && o->qk_fmt != VC_QK_MXFP4) return VC_ERR_UNSUPPORTED;
   if (o->p_mode != VC_P_EXPCAST && o->p_mode != VC_P_EXP_THEN_CAST) return VC_ERR_UNSUPPORTED;
   const int32_t flags[4] = {o->rope, o->hadamard, o->smooth_k, o->smooth_v};
   for (int32_t f : flags)
@@ -200,13 +200,15 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   if (st != VC_OK) return st;
   if ((st = check_opts(opts)) != VC_OK) return st;
   if (!Q || !K || !V || !out) return VC_ERR_NULL;
-  if (!out->q || !out->q_scale || !out->k || !out->k_scale || !out->k_mean || !out->v || !out->v_scale ||
-      !out->v_mean)
+  const bool mx = opts->qk_fmt == VC_QK_MXFP4;
+  // the per-block fp32 scales (INT8) or the E8M0 scale bytes (MXFP4)
+  const void* qsc = mx ? (const void*)out->q_mx_scale : (const void*)out->q_scale;
+  const void* ksc = mx ? (const void*)out->k_mx_scale : (const void*)out->k_scale;
+  if (!out->q || !qsc || !out->k || !ksc || !out->k_mean || !out->v || !out->v_scale || !out->v_mean)
     return VC_ERR_NULL;
   if (opts->rope && (!rope_cos || !rope_sin)) return VC_ERR_NULL;
   if (!ws || ws_bytes < prep_ws(shape)) return VC_ERR_WORKSPACE;
-  const void* ptrs[] = {Q, K, V, out->q, out->q_scale, out->k, out->k_scale, out->k_mean, out->v, out->v_scale,
-                        out->v_mean, ws};
+  const void* ptrs[] = {Q, K, V, out->q, qsc, out->k, ksc, out->k_mean, out->v, out->v_scale, out->v_mean, ws};
   for (const void* p : ptrs)
     if (!aligned16(p)) return VC_ERR_ALIGN;
   if ((perm && !aligned16(perm)) || (q_perm && !aligned16(q_perm)) || (rope_cos && !aligned16(rope_cos)) ||
@@ -247,6 +249,9 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   a.hadamard = opts->hadamard;
   a.smooth_k = opts->smooth_k;
   a.smooth_v = opts->smooth_v;
+  a.qk_fmt = opts->qk_fmt;
+  a.q_mxs = out->q_mx_scale;
+  a.k_mxs = out->k_mx_scale;
   return hip_status(vc::launch_prep(a, (int)BH, static_cast<hipStream_t>(stream)));
 }
 
@@ -256,8 +261,11 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
   if (st != VC_OK) return st;
   if ((st = check_opts(opts)) != VC_OK) return st;
   if (!in || !O) return VC_ERR_NULL;
-  if (!in->q || !in->q_scale || !in->k || !in->k_scale || !in->v || !in->v_scale || !in->v_mean) return VC_ERR_NULL;
-  const void* ptrs[] = {in->q, in->q_scale, in->k, in->k_scale, in->v, in->v_scale, in->v_mean, O};
+  const bool mx = opts->qk_fmt == VC_QK_MXFP4;
+  const void* qsc = mx ? (const void*)in->q_mx_scale : (const void*)in->q_scale;
+  const void* ksc = mx ? (const void*)in->k_mx_scale : (const void*)in->k_scale;
+  if (!in->q || !qsc || !in->k || !ksc || !in->v || !in->v_scale || !in->v_mean) return VC_ERR_NULL;
+  const void* ptrs[] = {in->q, qsc, in->k, ksc, in->v, in->v_scale, in->v_mean, O};
   for (const void* p : ptrs)
     if (!aligned16(p)) return VC_ERR_ALIGN;
   if (q_perm && !aligned16(q_perm)) return VC_ERR_ALIGN;
@@ -283,6 +291,9 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
   a.cbias = 120.0f + opts->beta;
   a.p_mode = opts->p_mode;
   a.smooth_v = opts->smooth_v;
+  a.qk_fmt = opts->qk_fmt;
+  a.q_mxs = in->q_mx_scale;
+  a.k_mxs = in->k_mx_scale;
   return hip_status(vc::launch_forward(a, (int)BH, static_cast<hipStream_t>(stream)));
 }
 

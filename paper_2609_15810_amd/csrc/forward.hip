@@ -37,6 +37,12 @@
 // steady-state loop is unrolled by four iterations so that every LDS access names its buffer
 // statically. Tiles are visited in ascending order with the running maximum updated once per
 // 128-key tile, the schedule on which the codes are defined.
+//
+// 4-bit variant (OCP MXFP4 Q and K): the scores come from the scaled FP4 product
+// v_mfma_scale_f32_32x32x64_f8f6f4 (two per 32-key block), each lane's E8M0 byte scaling its
+// 32-channel block, so S^T arrives in fp32 with the block scales applied and the score scale of
+// the codes is kappa alone. A K tile is 8 KB of packed codes followed by its 512 scale bytes;
+// everything after the scores is shared with the 8-bit path.
 #include <type_traits>
 
 #include "vc_common.hpp"
@@ -51,8 +57,13 @@ constexpr int NTH = 64 * NW;
 constexpr int NQ = 32 * NW;
 constexpr int TILE_BYTES = BLK * D;
 constexpr int VBUF_BYTES = TILE_BYTES + 2 * D;
-constexpr int KCOPIES = TILE_BYTES / 1024 / NW;  // 1 KB copies per wave per tile
+constexpr int KCOPIES = TILE_BYTES / 1024 / NW;  // 1 KB copies per wave per tile (V; INT8 K)
 constexpr int PAIR_COPIES = 2 * KCOPIES + 1;     // K and V pieces + the means
+constexpr int MX_CODE_BYTES = TILE_BYTES / 2;    // packed E2M1 codes of a 128-key tile
+constexpr int MX_SCALE_BYTES = BLK * D / 32;     // its E8M0 scale bytes, one per 32 channels
+static_assert(MX_CODE_BYTES / 1024 / NW == 1 && MX_SCALE_BYTES / NW <= 4 * 64,
+              "MXFP4 K tiles move as one 1 KB copy of codes and one 4-byte-per-lane copy of scales per wave");
+static_assert(MX_CODE_BYTES + MX_SCALE_BYTES <= TILE_BYTES, "an MXFP4 K tile fits a K buffer");
 constexpr int MEAN_LANES = 64 / NW;              // lanes copying 4 bytes of means each
 
 // s_waitcnt immediate for vmcnt(n) (bits 3:0 and 15:14), the other counters left at their maxima
@@ -81,6 +92,28 @@ __device__ __forceinline__ v4f mfma_f8_16(v8i a, v8i b, v4f c) {
 __device__ __forceinline__ int half_max(int v) {
   const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
   return max(max(v, (int)r[0]), (int)r[1]);
+}
+// fp32 version through the order-preserving map of fp32 bit patterns onto int32 (negative values
+// get their magnitude bits flipped; the map is its own inverse). Written this way because
+// fmaxf over the two outputs of the swap has been compiled into a max over one of them only.
+__device__ __forceinline__ float half_max(float v) {
+  const int b = __builtin_bit_cast(int, v);
+  const int m = half_max(b ^ ((b >> 31) & 0x7fffffff));
+  return __builtin_bit_cast(float, m ^ ((m >> 31) & 0x7fffffff));
+}
+__device__ __forceinline__ int smax(int a, int b) { return max(a, b); }
+__device__ __forceinline__ float smax(float a, float b) { return fmaxf(a, b); }
+__device__ __forceinline__ int smax3(int a, int b, int c) { return max(max(a, b), c); }
+__device__ __forceinline__ float smax3(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
+
+// Scaled FP4 x FP4 product (cbsz = blgp = 4): a, b hold 32 E2M1 codes per lane (one 32-channel
+// block of row / column l%32, channel block l/32 of the 64), scaled by byte OA of sa and byte OB
+// of sb (E8M0)
+template <int OA, int OB>
+__device__ __forceinline__ v16f mfma_f4(v4i a, v4i b, v16f c, int sa, int sb) {
+  const v8i a8 = __builtin_shufflevector(a, a, 0, 1, 2, 3, -1, -1, -1, -1);
+  const v8i b8 = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, OA, sa, OB, sb);
 }
 
 // Copies from global memory straight into LDS: lane l moves `bytes` bytes from base + voff to
@@ -119,13 +152,16 @@ __device__ __forceinline__ void pin(V& x) {
   asm volatile("" : "+v"(x));
 }
 
-// Padded keys of the last tile (key >= kvalid): INT_MIN scores before the softmax ...
-__device__ __forceinline__ void mask_tile(v16i (&s)[4], int kh, int kvalid) {
+// Padded keys of the last tile (key >= kvalid): the lowest score before the softmax ...
+template <typename SV>
+__device__ __forceinline__ void mask_tile(SV (&s)[4], int kh, int kvalid) {
+  using E = std::remove_reference_t<decltype(s[0][0])>;
+  constexpr E lowest = std::is_same_v<E, float> ? (E)-INFINITY : (E)INT_MIN;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      if (32 * kb + 8 * (r >> 2) + 4 * kh + (r & 3) >= kvalid) s[kb][r] = INT_MIN;
+      if (32 * kb + 8 * (r >> 2) + 4 * kh + (r & 3) >= kvalid) s[kb][r] = lowest;
 }
 
 // ... and zero probability codes after it.
@@ -144,9 +180,10 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
-template <int PMODE>
+template <int PMODE, bool MX>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_fwd(FwdArgs a) {
-  // K_t in kb[t % 4]; V_t with its 128 bf16 block means in vb[t % 4]; mu_t / s_V as bf16 hi + lo
+  using SV = std::conditional_t<MX, v16f, v16i>;  // a lane's 16 scores of one 32-key block
+  // K_t in kb[t % 4] (MXFP4: codes, then scale bytes at MX_CODE_BYTES); V_t with its 128 bf16 block means in vb[t % 4]; mu_t / s_V as bf16 hi + lo
   // in slot t % 8 of ub[(t / 8) % 2]; (r_t, m_t) per query in slot t % 8 of rm[wave]
   __shared__ __attribute__((aligned(16))) uint8_t kb0[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t kb1[TILE_BYTES];
@@ -169,12 +206,28 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 
   const int gq = NW * qt + wave;  // global 32-query group
   const int qblock = min(gq >> 2, T - 1);
-  const int8_t* qblk = a.q + (tile0 + qblock) * TILE_BYTES;
-  v4i qop[4];
+  const int qrb = gq & 3;         // the group's 32-row block within its 128-row block
+  // INT8: four 32-channel operands, scale sq per 128-row block; MXFP4: two 64-channel operands
+  // (each lane one 32-channel block of its query) with their E8M0 bytes qsc[m]
+  v4i qop[MX ? 2 : 4];
+  float sq = 1.f;
+  int qsc[2] = {0, 0};
+  if constexpr (MX) {
+    const uint8_t* qblk = reinterpret_cast<const uint8_t*>(a.q) + (tile0 + qblock) * MX_CODE_BYTES;
 #pragma unroll
-  for (int dc = 0; dc < 4; ++dc)
-    qop[dc] = *reinterpret_cast<const v4i*>(qblk + (((gq & 3) * 4 + dc) * 2 + kh) * 512 + col * 16);
-  const float sq = a.q_scale[tile0 + qblock];
+    for (int m = 0; m < 2; ++m)
+      qop[m] = *reinterpret_cast<const v4i*>(qblk + ((qrb * 2 + m) * 2 + kh) * 512 + col * 16);
+    const uint2 w = *reinterpret_cast<const uint2*>(a.q_mxs + (tile0 + qblock) * MX_SCALE_BYTES + lane * 8);
+    const uint32_t d = (qrb & 2) ? w.y : w.x;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) qsc[m] = (int)((d >> (8 * ((qrb & 1) * 2 + m))) & 0xffu);
+  } else {
+    const int8_t* qblk = a.q + (tile0 + qblock) * TILE_BYTES;
+#pragma unroll
+    for (int dc = 0; dc < 4; ++dc)
+      qop[dc] = *reinterpret_cast<const v4i*>(qblk + ((qrb * 4 + dc) * 2 + kh) * 512 + col * 16);
+    sq = a.q_scale[tile0 + qblock];
+  }
 
   const int mc = tid & (D - 1);
   if (tid < D) {
@@ -195,25 +248,33 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     ones16 = v8i{w, w, w, w, w, w, w, w};
   }
 
-  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + tile0 * TILE_BYTES;
+  constexpr int KT_BYTES = MX ? MX_CODE_BYTES : TILE_BYTES;  // K codes per tile in memory
+  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + tile0 * KT_BYTES;
+  const uint8_t* ksbase = MX ? a.k_mxs + tile0 * MX_SCALE_BYTES + (MX_SCALE_BYTES / NW) * wave : nullptr;
   const uint8_t* vbase = a.v + tile0 * TILE_BYTES;
   const uint8_t* mbase = reinterpret_cast<const uint8_t*>(a.v_mean + tile0 * D) + (2 * D / NW) * wave;
-  // K_t into kd: KCOPIES 1 KB copies per wave
+  // piece u < KCOPIES of K_t into kd (every piece one copy per wave). INT8: 1 KB of codes each;
+  // MXFP4: piece 0 = 1 KB of codes, piece 1 = MX_SCALE_BYTES / NW scale bytes
+  auto load_kpiece = [&](int u, int t, uint8_t* kd) __attribute__((always_inline)) {
+    if (!MX || u == 0) {
+      const int off = (u * NW + wave) * 1024;
+      copy16_to_lds(kbase + (size_t)t * KT_BYTES + off, lane * 16, lds_addr(kd + off));
+    } else if (lane < MX_SCALE_BYTES / NW / 4) {
+      copy4_to_lds(ksbase + (size_t)t * MX_SCALE_BYTES, 4 * lane,
+                   lds_addr(kd + MX_CODE_BYTES + (MX_SCALE_BYTES / NW) * wave));
+    }
+  };
   auto load_k = [&](int t, uint8_t* kd) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < KCOPIES; ++u) {
-      const int off = (u * NW + wave) * 1024;
-      copy16_to_lds(kbase + (size_t)t * TILE_BYTES + off, lane * 16, lds_addr(kd + off));
-    }
+    for (int u = 0; u < KCOPIES; ++u) load_kpiece(u, t, kd);
   };
   // copy k of pair p = (K_{p+2} clamped to the last tile, V_p with its means)
   auto load_part = [&](int k, int p, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
-    if (k < 2 * KCOPIES) {
-      const bool isk = k < KCOPIES;
-      const uint8_t* src = isk ? kbase + (size_t)min(p + 2, T - 1) * TILE_BYTES : vbase + (size_t)p * TILE_BYTES;
-      uint8_t* dst = isk ? kd : vd;
-      const int off = ((isk ? k : k - KCOPIES) * NW + wave) * 1024;
-      copy16_to_lds(src + off, lane * 16, lds_addr(dst + off));
+    if (k < KCOPIES) {
+      load_kpiece(k, min(p + 2, T - 1), kd);
+    } else if (k < 2 * KCOPIES) {
+      const int off = ((k - KCOPIES) * NW + wave) * 1024;
+      copy16_to_lds(vbase + (size_t)p * TILE_BYTES + off, lane * 16, lds_addr(vd + off));
     } else if (lane < MEAN_LANES) {
       copy4_to_lds(mbase + (size_t)p * 2 * D, 4 * lane, lds_addr(vd + TILE_BYTES + (2 * D / NW) * wave));
     }
@@ -223,7 +284,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     for (int k = 0; k < PAIR_COPIES; ++k) load_part(k, p, kd, vd);
   };
   const __attribute__((address_space(4))) float* kscale =
-      (const __attribute__((address_space(4))) float*)(a.k_scale + tile0);
+      (const __attribute__((address_space(4))) float*)(MX ? nullptr : a.k_scale + tile0);
   // mu_j / s_V as bf16 hi + lo into slot j % 8 of chunk parity (j / 8) % 2, from the means behind
   // V_j in vt (threads 0..127, one channel each)
   auto stash_mean = [&](int j, const uint8_t* vt) __attribute__((always_inline)) {
@@ -241,7 +302,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  v16i s[4];       // scores of the tile whose codes are computed next
+  SV s[4];         // scores of the tile whose codes are computed next
   v8i pc[2];       // codes of the tile whose value product is issued next
   float ksc = 0.f;  // scale of the K tile whose scores are in s
   float2* rm_q = &rm[wave][col][0];
@@ -278,33 +339,65 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   };
 
   // scores of tile t (K_t in kt) into s
+  // MXFP4 scores of key block kb from its two operands and the lane's scale dword kb/2 of the tile
+  auto qk_mx = [&](auto KBC, const v4i (&k)[2], int ksw) __attribute__((always_inline)) -> v16f {
+    constexpr int kb = decltype(KBC)::value;
+    v16f acc = {};
+    acc = mfma_f4<(kb & 1) * 2 + 0, 0>(k[0], qop[0], acc, ksw, qsc[0]);
+    acc = mfma_f4<(kb & 1) * 2 + 1, 0>(k[1], qop[1], acc, ksw, qsc[1]);
+    return acc;
+  };
+  auto mx_kops = [&](int kb, const uint8_t* kt, v4i (&k)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) k[m] = *reinterpret_cast<const v4i*>(kt + ((kb * 2 + m) * 2 + kh) * 512 + col * 16);
+  };
+  auto mx_scales = [&](const uint8_t* kt) __attribute__((always_inline)) -> uint2 {
+    return *reinterpret_cast<const uint2*>(kt + MX_CODE_BYTES + lane * 8);
+  };
+
+  // scores of tile t (K_t in kt) into s
   auto qk = [&](auto MASKC, int t, const uint8_t* kt) __attribute__((always_inline)) {
-    ksc = kscale[t];
+    if constexpr (MX) {
+      const uint2 ksw = mx_scales(kt);
+      v4i kops[2];
+      mx_kops(0, kt, kops);
+      s[0] = qk_mx(std::integral_constant<int, 0>{}, kops, (int)ksw.x);
+      mx_kops(1, kt, kops);
+      s[1] = qk_mx(std::integral_constant<int, 1>{}, kops, (int)ksw.x);
+      mx_kops(2, kt, kops);
+      s[2] = qk_mx(std::integral_constant<int, 2>{}, kops, (int)ksw.y);
+      mx_kops(3, kt, kops);
+      s[3] = qk_mx(std::integral_constant<int, 3>{}, kops, (int)ksw.y);
+    } else {
+      ksc = kscale[t];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      v4i kops[4];
+      for (int kb = 0; kb < 4; ++kb) {
+        v4i kops[4];
 #pragma unroll
-      for (int dc = 0; dc < 4; ++dc) kops[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
-      v16i acc = {};
+        for (int dc = 0; dc < 4; ++dc) kops[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
+        v16i acc = {};
 #pragma unroll
-      for (int dc = 0; dc < 4; ++dc) acc = mfma_i8(kops[dc], qop[dc], acc);
-      s[kb] = acc;
+        for (int dc = 0; dc < 4; ++dc) acc = mfma_i8(kops[dc], qop[dc], acc);
+        s[kb] = acc;
+      }
     }
     if (decltype(MASKC)::value) mask_tile(s, kh, a.N - (T - 1) * BLK);
   };
 
   // running maximum of tile t (scores in s) into m_new, alpha, codes into pn
   auto softmax = [&](auto LASTC, int t, v8i (&pn)[2], float& alpha, float& m_new) __attribute__((always_inline)) {
-    const float a_s = (sq * ksc) * a.kappa;  // the oracle's order: fl(fl(s_q s_k) kappa)
-    int mk[4];
+    // score scale a = fl(fl(s_q s_k) kappa) (INT8) or kappa (MXFP4: the block scales are inside s)
+    const float a_s = MX ? a.kappa : (sq * ksc) * a.kappa;
+    using E = std::remove_reference_t<decltype(s[0][0])>;
+    E mk[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      int m = max(s[kb][0], s[kb][1]);
+      E m = smax(s[kb][0], s[kb][1]);
 #pragma unroll
-      for (int r = 2; r < 16; r += 2) m = max(max(m, s[kb][r]), s[kb][r + 1]);
+      for (int r = 2; r < 16; r += 2) m = smax3(m, s[kb][r], s[kb][r + 1]);
       mk[kb] = m;
     }
-    int mx = max(max(mk[0], mk[1]), max(mk[2], mk[3]));
+    E mx = smax(smax(mk[0], mk[1]), smax(mk[2], mk[3]));
     mx = half_max(mx);
     m_new = fmaxf(m_run, (float)mx * a_s);
     alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -406,21 +499,36 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     auto hook = [&](int k) __attribute__((always_inline)) {
       if (cp && k < PAIR_COPIES) load_part(k, j + 3, kd, vd);
     };
-    auto kmax = [&](int kb) __attribute__((always_inline)) -> int {
-      int m = max(s[kb][0], s[kb][1]);
+    using E = std::remove_reference_t<decltype(s[0][0])>;
+    auto kmax = [&](int kb) __attribute__((always_inline)) -> E {
+      E m = smax(s[kb][0], s[kb][1]);
 #pragma unroll
-      for (int r = 2; r < 16; r += 2) m = max(max(m, s[kb][r]), s[kb][r + 1]);
+      for (int r = 2; r < 16; r += 2) m = smax3(m, s[kb][r], s[kb][r + 1]);
       return m;
     };
-    auto load_kops = [&](int kb, v4i (&k)[4]) __attribute__((always_inline)) {
+    // key operands of block kb (INT8: 4 x 32 channels; MXFP4: 2 x 64 channels and, with block 0,
+    // the lane's two scale dwords of the tile)
+    constexpr int NKOP = MX ? 2 : 4;
+    uint2 ksw = {0u, 0u};
+    auto load_kops = [&](int kb, v4i (&k)[NKOP]) __attribute__((always_inline)) {
+      if constexpr (MX) {
+        if (kb == 0) ksw = mx_scales(kt);
+        mx_kops(kb, kt, k);
+      } else {
 #pragma unroll
-      for (int dc = 0; dc < 4; ++dc) k[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
+        for (int dc = 0; dc < 4; ++dc) k[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
+      }
     };
-    auto qk_kb = [&](int kb, const v4i (&k)[4]) __attribute__((always_inline)) {
-      v16i acc = {};
+    auto qk_kb = [&](auto KBC, const v4i (&k)[NKOP]) __attribute__((always_inline)) {
+      constexpr int kb = decltype(KBC)::value;
+      if constexpr (MX) {
+        s[kb] = qk_mx(KBC, k, kb < 2 ? (int)ksw.x : (int)ksw.y);
+      } else {
+        v16i acc = {};
 #pragma unroll
-      for (int dc = 0; dc < 4; ++dc) acc = mfma_i8(k[dc], qop[dc], acc);
-      s[kb] = acc;
+        for (int dc = 0; dc < NKOP; ++dc) acc = mfma_i8(k[dc], qop[dc], acc);
+        s[kb] = acc;
+      }
     };
     v8i pn[2];
     float a8 = 0.f, bias = 0.f, a_s = 0.f, m_new = 0.f;
@@ -446,7 +554,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     };
     // at most 32 registers of operands staged at any time
     v8i va[2], vb[2];
-    v4i k0[4], k1[4];
+    v4i k0[NKOP], k1[NKOP];
     // R0: value operands 0, 1
     va[0] = load_vop(vt, 0);
     va[1] = load_vop(vt, 1);
@@ -458,7 +566,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     o[1] = mfma_f8(va[1], pc[0], o[1]);
     vb[0] = load_vop(vt, 2);
     vb[1] = load_vop(vt, 3);
-    int mk0 = kmax(0), mk1 = kmax(1);
+    E mk0 = kmax(0), mk1 = kmax(1);
     pin(mk0);
     pin(mk1);
     fence();
@@ -467,8 +575,8 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     o[3] = mfma_f8(vb[1], pc[0], o[3]);
     va[0] = load_vop(vt, 4);
     va[1] = load_vop(vt, 5);
-    a_s = (sq * ksc) * a.kappa;  // the oracle's order: fl(fl(s_q s_k) kappa)
-    int mx = max(max(mk0, mk1), max(kmax(2), kmax(3)));
+    a_s = MX ? a.kappa : (sq * ksc) * a.kappa;  // fl(fl(s_q s_k) kappa) for INT8
+    E mx = smax(smax(mk0, mk1), smax(kmax(2), kmax(3)));
     mx = half_max(mx);
     m_new = fmaxf(m_run, (float)mx * a_s);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -494,25 +602,25 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     load_kops(0, k0);
     o[2] = mfma_f8(vb[0], pc[1], o[2]);
     o[3] = mfma_f8(vb[1], pc[1], o[3]);
-    qk_kb(0, k0);
+    qk_kb(std::integral_constant<int, 0>{}, k0);
     codes_kb(1);
     hook(3);
     fence();
     // R5: scores of block 1; key operands of block 2; codes of block 2
     load_kops(1, k1);
-    qk_kb(1, k1);
+    qk_kb(std::integral_constant<int, 1>{}, k1);
     load_kops(2, k0);
     codes_kb(2);
     hook(4);
     fence();
     // R6: scores of block 2; key operands of block 3; codes of block 3
-    qk_kb(2, k0);
+    qk_kb(std::integral_constant<int, 2>{}, k0);
     load_kops(3, k1);
     codes_kb(3);
     fence();
     // R7: scores of block 3
-    qk_kb(3, k1);
-    ksc = kscale[j + 2];
+    qk_kb(std::integral_constant<int, 3>{}, k1);
+    if (!MX) ksc = kscale[j + 2];
     const float rsum = rs[0];
     if (a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
     rm_q[j & 7] = make_float2(rsum, m_run);
@@ -618,8 +726,14 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s) {
   const dim3 grid((a.N + NQ - 1) / NQ, BH);
-  if (a.p_mode == 0) attn_fwd<0><<<grid, NTH, 0, s>>>(a);
-  else attn_fwd<1><<<grid, NTH, 0, s>>>(a);
+  const bool mx = a.qk_fmt == VC_QK_MXFP4;
+  if (a.p_mode == 0) {
+    if (mx) attn_fwd<0, true><<<grid, NTH, 0, s>>>(a);
+    else attn_fwd<0, false><<<grid, NTH, 0, s>>>(a);
+  } else {
+    if (mx) attn_fwd<1, true><<<grid, NTH, 0, s>>>(a);
+    else attn_fwd<1, false><<<grid, NTH, 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 

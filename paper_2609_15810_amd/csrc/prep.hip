@@ -7,9 +7,9 @@
 //                 rows of original-order block j summed per channel (the centering statistics).
 //   prep_finalize grid (B*H, 16), 256 threads: key channel mean and per-channel value scale.
 //   prep_quant    grid (T, B*H, 3), 256 threads. z = 0: K' rows (gather, RoPE, centering,
-//                 Hadamard, per-block INT8); z = 1: V' rows (gather, demean, per-channel E4M3),
-//                 transposed into the tile order of the attention kernel; z = 2: Q rows (RoPE,
-//                 Hadamard, per-block INT8).
+//                 Hadamard, per-block INT8 or MXFP4); z = 1: V' rows (gather, demean, per-channel
+//                 E4M3), transposed into the tile order of the attention kernel; z = 2: Q rows
+//                 (RoPE, Hadamard, per-block INT8 or MXFP4).
 // All floating-point steps that decide a stored code are written as single IEEE fp32
 // operations in a fixed order (compiled with -ffp-contract=off; fused multiply-adds are spelled
 // out), so the codes, scales and means are reproducible bit for bit.
@@ -460,10 +460,23 @@ __device__ __forceinline__ void rope_row32(float (&x)[4][8], int n, int k4, cons
   }
 }
 
+// Nearest E2M1 (MX FP4) code of v, |v| < 8: ties to the code with mantissa bit 0, saturating at
+// 6, +0 for magnitudes that round to 0. With a = |v|, the code magnitude is rint(2a) below 2,
+// 4 + rint(a - 2) on [2, 4) and 6 + rint((a - 4) / 2) on [4, 8) (each argument exact, so rint's
+// ties to even are the format's ties), capped at 7.
+__device__ __forceinline__ uint32_t fp4_code(float v) {
+  const float a = fabsf(v);
+  const float t = a < 2.f ? 2.f * a : (a < 4.f ? a - 2.f : __builtin_fmaf(a, 0.5f, -2.f));
+  const float base = a < 2.f ? 0.f : (a < 4.f ? 4.f : 6.f);
+  const uint32_t mag = (uint32_t)fminf(base + __builtin_rintf(t), 7.f);
+  return mag | ((v < 0.f && mag != 0u) ? 8u : 0u);
+}
+
 // Q (IS_K = false) or K' (IS_K = true) rows of block j: gather, RoPE, centering (K), Hadamard,
-// per-block symmetric INT8 (scale = amax/127, code = rint(x * (127/amax))).
-template <bool IS_K, bool ROPE, bool HAD>
-__device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red) {
+// then either per-block symmetric INT8 (scale = amax/127, code = rint(x * (127/amax))) or, with
+// MX, MXFP4 by 32-channel blocks (E8M0 scale byte floor(log2(amax)) - 2 + 127 per block).
+template <bool IS_K, bool ROPE, bool HAD, bool MX>
+__device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red, uint8_t* stage) {
   const int j = blockIdx.x, bh = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, k4 = lane & 3;
   const int r0 = j * BLK;
@@ -500,6 +513,40 @@ __device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red) {
         for (int e = 0; e < 8; ++e) x[it][i][e] = 0.f;
   }
 
+  const float sigma = HAD ? (((k4 ^ (k4 >> 1)) & 1) ? -1.f : 1.f) : 1.f;
+  if constexpr (MX) {
+    // channels 32 i .. 32 i + 31 of a row (one MX block) sit in the 4 lanes of the row's quad,
+    // 8 each; lane (h*32 + r) of the scaled product's operand = row r, block 2m + h
+    uint8_t* codes = reinterpret_cast<uint8_t*>(IS_K ? a.k : a.q) + ((size_t)bh * a.T + j) * (BLK * D / 2);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int rl = wave * 32 + it * 16 + (lane >> 2), rb = rl >> 5, r = rl & 31;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float m = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(x[it][i][e]));
+        m = fmaxf(m, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, m), 0xb1, 0xf, 0xf, true)));
+        m = fmaxf(m, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, m), 0x4e, 0xf, 0xf, true)));
+        // floor(log2(m)) = exponent field - 127 for normal m; subnormal m clamps to byte 0
+        const int ef = (int)((__float_as_uint(m) >> 23) & 0xffu);
+        const int sb = m > 0.f ? max(ef - 2, 0) : 127;
+        // sigma * 2^-X (exact scaling; the carried Hadamard sign restored)
+        const float mult = sigma * __uint_as_float((uint32_t)(254 - sb) << 23);
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w |= fp4_code(x[it][i][e] * mult) << (4 * e);
+        const int mm = i >> 1, hh = i & 1;
+        *reinterpret_cast<uint32_t*>(codes + ((rb * 2 + mm) * 2 + hh) * 512 + r * 16 + 4 * k4) = w;
+        if (k4 == 0) stage[(hh * 32 + r) * 8 + rb * 2 + mm] = (uint8_t)sb;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < 128)
+      reinterpret_cast<uint32_t*>((IS_K ? a.k_mxs : a.q_mxs) + ((size_t)bh * a.T + j) * 512)[threadIdx.x] =
+          reinterpret_cast<const uint32_t*>(stage)[threadIdx.x];
+    return;
+  }
   float m = 0.f;
 #pragma unroll
   for (int it = 0; it < 2; ++it)
@@ -517,7 +564,6 @@ __device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red) {
   // exactly s * fl(x inv). |fl(x inv)| <= 127 (1 + 2^-24)^2 < 127.5, so adding 1.5 * 2^23 rounds
   // it to the nearest integer, ties to even (the oracle's rint; its clamp to +-127 never acts),
   // and the low byte of the sum's bits is that integer in two's complement.
-  const float sigma = HAD ? (((k4 ^ (k4 >> 1)) & 1) ? -1.f : 1.f) : 1.f;
   const float mult = sigma * inv;
   int8_t* codes = (IS_K ? a.k : a.q) + ((size_t)bh * a.T + j) * (BLK * D);
 #pragma unroll
@@ -591,17 +637,18 @@ __device__ __forceinline__ void quant_v(const PrepArgs& a, uint8_t (*vt)[D + 8])
 }
 
 // grid (T, B*H, 3): z = 0 K' rows, z = 1 V' rows, z = 2 Q rows of block blockIdx.x.
-template <bool ROPE, bool HAD>
+template <bool ROPE, bool HAD, bool MX>
 __global__ __launch_bounds__(256) void prep_quant(PrepArgs a) {
   __shared__ float red[4];
-  __shared__ uint8_t vt[BLK][D + 8];  // V codes of the block, row-major (8-byte rows), for the transpose
+  // V codes of the block, row-major (8-byte rows), for the transpose; MX scale bytes of a Q/K block
+  __shared__ uint8_t vt[BLK][D + 8];
   // K' and V' first: their rows were just read by the statistics pass and may still be cached
   if (blockIdx.z == 0)
-    quant_qk<true, ROPE, HAD>(a, red);
+    quant_qk<true, ROPE, HAD, MX>(a, red, &vt[0][0]);
   else if (blockIdx.z == 1)
     quant_v(a, vt);
   else
-    quant_qk<false, ROPE, HAD>(a, red);
+    quant_qk<false, ROPE, HAD, MX>(a, red, &vt[0][0]);
 }
 
 hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
@@ -612,17 +659,24 @@ hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
     prep_stats<false><<<sgrid, 64, 0, s>>>(a);
   prep_finalize<<<dim3(BH, 16), 256, 0, s>>>(a);
   const dim3 grid(a.T, BH, 3);
-  if (a.rope) {
-    if (a.hadamard)
-      prep_quant<true, true><<<grid, 256, 0, s>>>(a);
-    else
-      prep_quant<true, false><<<grid, 256, 0, s>>>(a);
-  } else {
-    if (a.hadamard)
-      prep_quant<false, true><<<grid, 256, 0, s>>>(a);
-    else
-      prep_quant<false, false><<<grid, 256, 0, s>>>(a);
-  }
+  auto quant = [&](auto MXC) {
+    constexpr bool mx = decltype(MXC)::value;
+    if (a.rope) {
+      if (a.hadamard)
+        prep_quant<true, true, mx><<<grid, 256, 0, s>>>(a);
+      else
+        prep_quant<true, false, mx><<<grid, 256, 0, s>>>(a);
+    } else {
+      if (a.hadamard)
+        prep_quant<false, true, mx><<<grid, 256, 0, s>>>(a);
+      else
+        prep_quant<false, false, mx><<<grid, 256, 0, s>>>(a);
+    }
+  };
+  if (a.qk_fmt == VC_QK_MXFP4)
+    quant(std::integral_constant<bool, true>{});
+  else
+    quant(std::integral_constant<bool, false>{});
   return hipGetLastError();
 }
 

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "vc_attn.h"
+
 namespace vc {
 
 struct PrepArgs {
@@ -17,12 +19,14 @@ struct PrepArgs {
   uint8_t* v;
   float* v_scale;
   uint16_t* v_mean;
+  uint8_t *q_mxs, *k_mxs;  // E8M0 scale bytes (MXFP4 only)
   float* ws_ksum;   // [B*H][T][128] per-block key channel sums
   float* ws_vamax;  // [B*H][T][128] per-block residual maxima
   float* ws_vinv;   // [B*H][128]    448 / amax (0 for an all-zero channel)
   int N, T, F, Ht, Wd;
   float inv_w, inv_hw;  // 1/Wd and 1/(Ht*Wd) in fp32: estimates for the token-position divisions
   int rope, hadamard, smooth_k, smooth_v;
+  int qk_fmt;
 };
 
 struct FwdArgs {
@@ -33,12 +37,14 @@ struct FwdArgs {
   const uint8_t* v;
   const float* v_scale;
   const uint16_t* v_mean;
+  const uint8_t *q_mxs, *k_mxs;  // E8M0 scale bytes (MXFP4 only)
   const int32_t* q_perm;
   uint16_t* O;
   int N, T;
   float kappa;      // sm_scale * log2(e) (/ 128 with the Hadamard rotation), rounded once to fp32
   float cbias;      // fl(120 + beta)
   int p_mode, smooth_v;
+  int qk_fmt;
 };
 
 struct GroupArgs {

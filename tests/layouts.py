@@ -35,3 +35,41 @@ def untile_qk(phys):
 
 def untile_v(phys):
     return untile(phys, V_INDEX)
+
+
+def _mx_code_index():
+    """byte index and nibble shift of channel ch of row `row` in a packed MXFP4 block:
+    [rb 4][m 2][h 2][r 32][16 bytes], two channels per byte (even channel in the low nibble)."""
+    row = np.arange(128)[:, None]
+    ch = np.arange(128)[None, :]
+    rb, r, m, h = row // 32, row % 32, ch // 64, (ch % 64) // 32
+    byte = ((rb * 2 + m) * 2 + h) * 512 + r * 16 + (ch % 32) // 2
+    return byte, np.broadcast_to(4 * (ch % 2), byte.shape)
+
+
+def _mx_scale_index():
+    """position of the E8M0 byte of row `row`, 32-channel block b (b = 2m + h) in the 512 scale
+    bytes of a block: [lane 64][rb 4][m 2] with lane = 32h + r."""
+    row = np.arange(128)[:, None]
+    b = np.arange(4)[None, :]
+    rb, r, m, h = row // 32, row % 32, b // 2, b % 2
+    return (h * 32 + r) * 8 + rb * 2 + m
+
+
+MX_CODE_BYTE, MX_CODE_SHIFT = _mx_code_index()
+MX_SCALE_INDEX = _mx_scale_index()
+
+
+def untile_mx_codes(phys: np.ndarray) -> np.ndarray:
+    """phys: [..., Np, 64] packed bytes -> one E2M1 code per byte [..., Np, 128]."""
+    shp = phys.shape
+    blocks = phys.reshape(-1, 128 * 64).astype(np.uint8)
+    out = (blocks[:, MX_CODE_BYTE.reshape(-1)] >> MX_CODE_SHIFT.reshape(-1).astype(np.uint8)) & 15
+    return out.reshape(shp[:-1] + (128,))
+
+
+def untile_mx_scales(phys: np.ndarray) -> np.ndarray:
+    """phys: [..., Np, 4] scale bytes in the library's order -> [..., Np, 4] by (row, block)."""
+    shp = phys.shape
+    blocks = phys.reshape(-1, 128 * 4).astype(np.uint8)
+    return blocks[:, MX_SCALE_INDEX.reshape(-1)].reshape(shp)

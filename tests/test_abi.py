@@ -72,6 +72,11 @@ def test_prep_validation(L):
     assert prep_call(L, shape(), o, ptrs=P) == 1
     P = vc.Prepped(*([FAKE] * 8)); P.k = FAKE + 4
     assert prep_call(L, shape(), o, ptrs=P) == 5
+    # MXFP4: the E8M0 scale buffers replace the fp32 block scales, which may then be NULL
+    mx = vc.make_opts(qk_fmt=vc.QK_MXFP4)
+    assert prep_call(L, shape(), mx) == 1                      # q_mx_scale / k_mx_scale NULL
+    P = vc.Prepped(*([FAKE] * 10)); P.q_scale = P.k_scale = None; P.k_mx_scale = FAKE + 8
+    assert prep_call(L, shape(), mx, ptrs=P) == 5              # past the NULL check: misaligned
     # RoPE tables are required only with rope = 1
     assert L.vc_attn_prep(C.byref(shape()), C.byref(o), FAKE, FAKE, FAKE, None, None, None, None,
                           C.byref(vc.Prepped(*([FAKE] * 8))), FAKE, 1 << 30, None) == 1
@@ -83,6 +88,10 @@ def test_forward_and_group_validation(L):
     assert L.vc_attn_forward(C.byref(shape(Wd=15)), C.byref(o), C.byref(P), None, FAKE, None) == 2
     assert L.vc_attn_forward(C.byref(shape()), C.byref(o), C.byref(P), None, None, None) == 1
     assert L.vc_attn_forward(C.byref(shape()), C.byref(o), C.byref(P), FAKE + 2, FAKE, None) == 5
+    mx = vc.make_opts(qk_fmt=vc.QK_MXFP4)
+    assert L.vc_attn_forward(C.byref(shape()), C.byref(mx), C.byref(P), FAKE, FAKE, None) == 1
+    P10 = vc.Prepped(*([FAKE] * 10)); P10.q_scale = P10.k_scale = None; P10.q_mx_scale = FAKE + 4
+    assert L.vc_attn_forward(C.byref(shape()), C.byref(mx), C.byref(P10), FAKE, FAKE, None) == 5
     g = vc.make_group_opts(k=65)
     assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 3
     g = vc.make_group_opts(iters=-1)
