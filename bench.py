@@ -14,7 +14,9 @@ the same workload on the host cores (and the same sample gives the parity number
 
 Beside the main line: `loop_slice`, the denoising-loop slice (8 calls of the same shape with
 interpolated inputs, grouping on calls 0 and 4) with prep GB/s, attention TOPS and the amortized
-grouping share; `large_layer`, the 75600-token 40-head layer timed stage by stage.
+grouping share; `large_layer`, the 75600-token 40-head layer timed stage by stage; `mx4_layer`,
+the 4-bit variant (MXFP4 Q/K, FP8 P/V) on the 32760-token 40-head layer beside the 8-bit path on the
+same inputs and permutation, timed, and (with the CPU leg) both compared with exact fp64 attention.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra]
 """
@@ -35,6 +37,9 @@ sys.path.insert(0, ROOT)
 METRIC = "quantized attention effective TOPS (N=32760,d=128) + % 8-bit MFMA peak; rel-L2"
 PEAK_8BIT_TOPS = 5000.0   # MI355X dense INT8 / OCP-FP8 matrix peak (5.0 POP/s)
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E
+PEAK_FP4_TOPS = 10100.0   # MI355X dense MXFP4 matrix peak
+# 4-bit attention: half the operations at the FP4 rate (scores), half at the FP8 rate (values)
+PEAK_MX4_MIXED_TOPS = 2.0 / (1.0 / PEAK_FP4_TOPS + 1.0 / PEAK_8BIT_TOPS)
 WORKLOAD = "dit_small"
 ATTN_KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_15810_amd", "csrc", "forward.hip")
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fwd_dit_small_counters.json")
@@ -178,6 +183,59 @@ def large_layer(vc, S, reps=3):
             "prep_frac_hbm": prep_algorithmic_bytes(B, H, N) / (t_prep * 1e-3) / 1e9 / PEAK_HBM_GBS}
 
 
+def mx4_layer(vc, S, reps=5):
+    """4-bit variant (MXFP4 Q/K after the Hadamard rotation, ExpCast-FP8 P, FP8 V) on the
+    32760-token 40-head layer, with the 8-bit path on the same inputs and the same k-means
+    permutation: preprocessing and attention timed per format; returns the GPU outputs of a few
+    heads on sampled query rows for the accuracy comparison."""
+    import torch
+    name = "dit_small_h40"
+    w = S.WORKLOADS[name]
+    B, H, N = w.B, w.H, w.N
+    Qh, Kh, Vh = S.make_qkv(name, seed=0)
+    Q, K, V = (torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).cuda() for x in (Qh, Kh, Vh))
+    O = torch.empty((B, H, N, 128), dtype=torch.int16, device="cuda")
+    heads = [0, 13, 39]
+    T = (N + 127) // 128
+    rows = np.concatenate([np.arange(128 * b, min(N, 128 * b + 128)) for b in (0, T // 2, T - 1)]).astype(np.int32)
+    ops = 4.0 * B * H * N * N * 128
+    res = {"workload": f"B={B} H={H} N={N} (grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]}) d=128, k-means k=32 8 rounds",
+           "sample_heads": heads, "sample_rows": int(rows.size)}
+    perm, samples = None, {}
+    for fmt, tag in ((vc.QK_MXFP4, "mxfp4"), (vc.QK_INT8, "int8")):
+        A = vc.Attention(B, H, w.grid, vc.make_opts(qk_fmt=fmt))
+        if perm is None:
+            A.group(V)
+            perm = A.perm.clone()
+        else:
+            A.perm.copy_(perm)
+        fns = [lambda: A.prep(Q, K, V), lambda: A.forward(O)]
+        time_stages(fns, 1)
+        t_prep, t_attn = time_stages(fns, reps)
+        tops = ops / (t_attn * 1e-3) / 1e12
+        peak = PEAK_MX4_MIXED_TOPS if fmt == vc.QK_MXFP4 else PEAK_8BIT_TOPS
+        res[tag] = {"prep_ms": t_prep, "attn_ms": t_attn, "attention_tops": tops, "peak_tops": peak,
+                    "attention_frac_peak": tops / peak}
+        o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(B * H, N, 128)
+        samples[tag] = o[heads][:, rows].astype(np.float64)
+    res["peak_note"] = ("mxfp4 peak: half the operations at the FP4 rate (10.1 POP/s) and half at the FP8 rate "
+                        "(5.0 POP/s), 2 / (1/10.1 + 1/5.0) = 6.69 POP/s")
+    return res, (Qh, Kh, Vh, w.grid, heads, rows, samples)
+
+
+def mx4_accuracy(sample):
+    """rel-L2 and PSNR of both formats' GPU outputs against exact fp64 attention (oracle) on the
+    sampled rows."""
+    import oracle
+    Qh, Kh, Vh, grid, heads, rows, samples = sample
+    exact = oracle.reference_attention(Qh[:, heads], Kh[:, heads], Vh[:, heads], grid, rows)
+    out = {}
+    for tag, o in samples.items():
+        out[tag] = {"rel_l2_vs_fp64": float(np.linalg.norm(o - exact) / np.linalg.norm(exact)),
+                    "psnr_vs_fp64_db": float(10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2)))}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,12 +337,18 @@ def main():
         out["loop_slice"] = loop_slice(vc, S)
         print("[bench] large layer", file=sys.stderr, flush=True)
         out["large_layer"] = large_layer(vc, S)
+        print("[bench] 4-bit variant layer", file=sys.stderr, flush=True)
+        out["mx4_layer"], mx4_sample = mx4_layer(vc, S)
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle sample", file=sys.stderr, flush=True)
         O_host = S.bits_to_f32(O.cpu().numpy().view(np.uint16))
         r = cpu_baseline(Q, K, V, grid, O_host.reshape(B * H, N, 128))
         out["cpu_baseline"] = r["baseline"]
         out["parity"] = r["parity"]
+        if not args.no_extra:
+            print("[bench] 4-bit variant accuracy against fp64", file=sys.stderr, flush=True)
+            for tag, acc in mx4_accuracy(mx4_sample).items():
+                out["mx4_layer"][tag].update(acc)
     print(json.dumps(out), flush=True)
 
 

@@ -156,3 +156,59 @@ def test_loop_slice_warm_regroup():
     assert_prep_equal(host_prepped(A), pp, "loop call 4")
     rows = sample_rows(w.N)
     check_output(o[:, rows], oracle.attention(pp, rows), "loop call 4")
+
+
+def host_prepped_mx(A):
+    from layouts import untile_mx_codes, untile_mx_scales
+    pp = A.prepped
+    u8 = lambda t: t.cpu().numpy().view(np.uint8)
+    return dict(q_mx=untile_mx_codes(u8(pp.q)), q_mxs=untile_mx_scales(u8(pp.q_mx_scale)),
+                k_mx=untile_mx_codes(u8(pp.k)), k_mxs=untile_mx_scales(u8(pp.k_mx_scale)),
+                v=untile_v(pp.v.cpu().numpy()), v_mean=pp.v_mean.cpu().numpy().view(np.uint16),
+                k_mean=pp.k_mean.cpu().numpy(), v_scale=pp.v_scale.cpu().numpy())
+
+
+@pytest.mark.timeout(900)
+def test_mx4_h40_full_vs_8bit():
+    """4-bit variant at the 32760-token, 40-head shape: MXFP4 codes and scales of every head
+    bit-exact, attention on sampled rows of three heads within the tolerance, and both the 4-bit
+    and the 8-bit GPU outputs compared with exact fp64 attention (reported; the 4-bit error is
+    below a loose bound and larger than the 8-bit one)."""
+    name = "dit_small_h40"
+    w = S.WORKLOADS[name]
+    log("generating inputs")
+    Q, K, V = S.make_qkv(name, seed=0)
+    log("oracle grouping (its permutation drives both sides)")
+    g = oracle.group(V, w.grid, k=32, iters=8)
+    perm = torch.from_numpy(np.ascontiguousarray(g["perm"])).cuda()
+    outs = {}
+    for fmt in (vc.QK_MXFP4, vc.QK_INT8):
+        log(f"GPU prep + forward, qk_fmt={fmt}")
+        A = vc.Attention(w.B, w.H, w.grid, vc.make_opts(qk_fmt=fmt))
+        A.perm.copy_(perm)
+        A, outs[fmt] = run_gpu(name, Q, K, V, A=A, regroup=False)
+        if fmt == vc.QK_MXFP4:
+            g_mx = host_prepped_mx(A)
+    log("oracle MXFP4 preprocessing (40 heads)")
+    pp = oracle.prep(Q, K, V, w.grid, perm=g["perm"], qk_fmt=oracle.QK_MXFP4)
+    for key in ("q_mx", "q_mxs", "k_mx", "k_mxs", "v", "v_mean"):
+        assert np.array_equal(g_mx[key], pp[key]), key
+    for key in ("k_mean", "v_scale"):
+        assert np.array_equal(f32_bits(g_mx[key]), f32_bits(pp[key])), key
+    del pp
+    rows = sample_rows(w.N)
+    heads = [0, 13, 39]
+    log(f"oracle MXFP4 attention on {rows.size} rows x {len(heads)} heads")
+    pph = oracle.prep(Q[:, heads], K[:, heads], V[:, heads], w.grid, perm=g["perm"][:, heads], qk_fmt=oracle.QK_MXFP4)
+    check_output(outs[vc.QK_MXFP4][heads][:, rows], oracle.attention(pph, rows), name + " mxfp4")
+    log("exact fp64 attention on the same rows")
+    exact = oracle.reference_attention(Q[:, heads], K[:, heads], V[:, heads], w.grid, rows)
+    rel = {}
+    for fmt, tag in ((vc.QK_MXFP4, "mxfp4"), (vc.QK_INT8, "int8")):
+        o = outs[fmt][heads][:, rows]
+        rel[tag] = np.linalg.norm(o - exact) / np.linalg.norm(exact)
+        psnr = 10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2))
+        log(f"{tag}: rel-L2 vs fp64 {rel[tag]:.4e}, PSNR {psnr:.2f} dB")
+    # loose sanity bound: on this shape the 4-bit scores leave about 14% rel-L2 (PSNR ~43 dB) against
+    # ~1.1% (~65 dB) for the 8-bit path
+    assert rel["mxfp4"] < 0.25 and rel["int8"] < rel["mxfp4"], rel
