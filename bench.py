@@ -18,7 +18,7 @@ grouping share; `large_layer`, the 75600-token 40-head layer timed stage by stag
 the 4-bit variant (MXFP4 Q/K, FP8 P/V) on the 32760-token 40-head layer beside the 8-bit path on the
 same inputs and permutation, timed, and (with the CPU leg) both compared with exact fp64 attention.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra] [--mx4-only]
 """
 from __future__ import annotations
 
@@ -244,6 +244,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the denoising-loop slice and the large layer (reported beside the main line)")
+    ap.add_argument("--mx4-only", action="store_true",
+                    help="run only the 4-bit variant block (for kernel traces of that shape) and print it")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -260,6 +262,14 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.mx4_only:
+        res, _ = mx4_layer(vc, S, reps=args.steps)
+        if args.calib_copy_mib:
+            src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+            torch.empty_like(src).copy_(src)
+            torch.cuda.synchronize()
+        print(json.dumps({"mx4_layer": res}), flush=True)
+        return
     w = S.WORKLOADS[WORKLOAD]
     B, H, N, grid = w.B, w.H, w.N, w.grid
     print(f"[bench] generating {WORKLOAD} inputs B={B} H={H} N={N}", file=sys.stderr, flush=True)
