@@ -44,7 +44,7 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
-QK_INT8, QK_MXFP4 = 0, 2
+QK_INT8, QK_FP8, QK_MXFP4 = 0, 1, 2
 
 
 class PrepCfg(C.Structure):
@@ -202,7 +202,7 @@ def prep(Q, K, V, grid, perm=None, q_perm=None, rope=True, hadamard=True, smooth
     """Q, K, V: uint16 bf16 bits [B, H, N, 128]. perm / q_perm: int32 [B, H, N] or None.
 
     Returns a dict of numpy arrays (see ``or_prep_head`` in vc_oracle.c for the layouts); with
-    qk_fmt = QK_MXFP4 also q_mx / k_mx (one E2M1 code per byte [B, H, Np, 128]) and q_mxs / k_mxs
+    qk_fmt = QK_FP8, q and k hold E4M3 bytes (uint8) with scales amax/448; with qk_fmt = QK_MXFP4 also q_mx / k_mx (one E2M1 code per byte [B, H, Np, 128]) and q_mxs / k_mxs
     (E8M0 scale bytes [B, H, Np, 4]).
     """
     Q, K, V = (_c(t, np.uint16) for t in (Q, K, V))
@@ -234,6 +234,8 @@ def prep(Q, K, V, grid, perm=None, q_perm=None, rope=True, hadamard=True, smooth
                        _p(out.get("k_mxs")))
     if rc != 0:
         raise MemoryError("oracle prep failed")
+    if qk_fmt == QK_FP8:
+        out["q"], out["k"] = out["q"].view(np.uint8), out["k"].view(np.uint8)
     out.update(N=N, grid=(F, Ht, Wd), hadamard=bool(hadamard), smooth_v=bool(smooth_v), qk_fmt=int(qk_fmt))
     return out
 
@@ -264,8 +266,8 @@ def attention(pp, rows, bh=None, p_mode=P_EXPCAST, sm_scale=None, beta=-0.35):
     for t, h in enumerate(bh):
         o = np.zeros((rows.size, D), np.float64)
         mxargs = [_p(_c(a[h], np.uint8)) for a in (qm, qms, km, kms)] if mx else [None] * 4
-        lib().or_attn_head(C.byref(cfg), _p(_c(q[h], np.int8)), _p(_c(qs[h], np.float32)),
-                           _p(_c(k[h], np.int8)), _p(_c(ks[h], np.float32)), _p(_c(v[h], np.uint8)),
+        lib().or_attn_head(C.byref(cfg), _p(_c(q[h].view(np.int8), np.int8)), _p(_c(qs[h], np.float32)),
+                           _p(_c(k[h].view(np.int8), np.int8)), _p(_c(ks[h], np.float32)), _p(_c(v[h], np.uint8)),
                            _p(_c(vs[h], np.float32)), _p(_c(vm[h], np.uint16)), C.c_int(rows.size),
                            _p(rows), _p(o), *mxargs)
         out[t] = o

@@ -315,6 +315,27 @@ static void quant_block_mx(const float *x, int valid, uint8_t *codes, uint8_t *s
         for (int b = 0; b < 4; ++b) or_mx_block(&x[r * D + 32 * b], &codes[r * D + 32 * b], &scales[r * 4 + b]);
 }
 
+/* FP8 Q/K (READING: the FP8-QK variant of Sec. 4.5 for matrix units without INT8): symmetric
+ * OCP E4M3 codes per 128-row block, like the INT8 quantizer with 448 (the largest finite E4M3
+ * value) in place of 127: scale = amax / 448, code = E4M3 nearest-even encoding of
+ * fl(x * fl(448 / amax)) (at most 448 up to one rounding, so the encoder's saturation decides
+ * nothing); all-zero block: scale 1, codes 0; padded rows: code 0. */
+static void quant_block_f8(const float *x, int valid, uint8_t *codes, float *scale)
+{
+    float amax = 0.0f;
+    for (int r = 0; r < valid; ++r)
+        for (int c = 0; c < D; ++c) {
+            float v = fabsf(x[r * D + c]);
+            if (v > amax) amax = v;
+        }
+    memset(codes, 0, (size_t)BLK * D);
+    if (amax == 0.0f) { *scale = 1.0f; return; }
+    float inv = 448.0f / amax;
+    *scale = amax / 448.0f;
+    for (int r = 0; r < valid; ++r)
+        for (int c = 0; c < D; ++c) codes[r * D + c] = or_e4m3_encode(x[r * D + c] * inv);
+}
+
 /* The score of one query row against one key row from their MX codes, exact (fp64):
  * sum over the four blocks of 2^(Xq + Xk) times the block's dot product of the decoded elements. */
 double or_mx_score(const uint8_t *q, const uint8_t *qs, const uint8_t *k, const uint8_t *ks)
@@ -332,12 +353,12 @@ double or_mx_score(const uint8_t *q, const uint8_t *qs, const uint8_t *k, const 
 /* Preprocessing of one (batch, head): Q, K, V -> codes, scales, means (Sec. 3.4, App. B)     */
 /* ------------------------------------------------------------------------------------------ */
 
-enum { OR_QK_INT8 = 0, OR_QK_MXFP4 = 2 };
+enum { OR_QK_INT8 = 0, OR_QK_FP8 = 1, OR_QK_MXFP4 = 2 };
 
 typedef struct {
     int32_t N, F, Ht, Wd;
     int32_t rope, hadamard, smooth_k, smooth_v;
-    int32_t qk_fmt;  /* OR_QK_INT8 or OR_QK_MXFP4 */
+    int32_t qk_fmt;  /* OR_QK_INT8, OR_QK_FP8 or OR_QK_MXFP4 */
 } or_prep_cfg;
 
 /* Inputs: Q, K, V as bf16 bit patterns [N x 128] in token order; perm (K/V gather, NULL =
@@ -348,6 +369,7 @@ typedef struct {
  *   k_mean  fp32 [128]                            (zeros when smooth_k = 0)
  *   v_codes E4M3 bytes [Np x 128], v_scale [128]  (permuted order, residual after demeaning)
  *   v_mean  bf16 bits [T x 128]                   (zeros when smooth_v = 0)
+ * With qk_fmt = OR_QK_FP8 q_codes / k_codes hold E4M3 bytes (same layout, scales amax/448).
  * With qk_fmt = OR_QK_MXFP4 the Q and K rows are quantized by MX blocks instead (the INT8
  * outputs are not written): q_mx, k_mx one E2M1 code per byte [Np x 128], q_mxs, k_mxs E8M0
  * scale bytes [Np x 4].
@@ -378,6 +400,8 @@ int or_prep_head(const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, c
         int valid = N - j * BLK < BLK ? N - j * BLK : BLK;
         if (mx)
             quant_block_mx(&xq[(size_t)j * BLK * D], valid, &q_mx[(size_t)j * BLK * D], &q_mxs[(size_t)j * BLK * 4]);
+        else if (cfg->qk_fmt == OR_QK_FP8)
+            quant_block_f8(&xq[(size_t)j * BLK * D], valid, (uint8_t *)&q_codes[(size_t)j * BLK * D], &q_scale[j]);
         else
             quant_block_i8(&xq[(size_t)j * BLK * D], valid, &q_codes[(size_t)j * BLK * D], &q_scale[j]);
     }
@@ -417,6 +441,8 @@ int or_prep_head(const or_prep_cfg *cfg, const uint16_t *Q, const uint16_t *K, c
         int valid = N - j * BLK < BLK ? N - j * BLK : BLK;
         if (mx)
             quant_block_mx(&xk[(size_t)j * BLK * D], valid, &k_mx[(size_t)j * BLK * D], &k_mxs[(size_t)j * BLK * 4]);
+        else if (cfg->qk_fmt == OR_QK_FP8)
+            quant_block_f8(&xk[(size_t)j * BLK * D], valid, (uint8_t *)&k_codes[(size_t)j * BLK * D], &k_scale[j]);
         else
             quant_block_i8(&xk[(size_t)j * BLK * D], valid, &k_codes[(size_t)j * BLK * D], &k_scale[j]);
     }
@@ -475,7 +501,7 @@ enum { OR_P_EXPCAST = 0, OR_P_EXP_THEN_CAST = 1 };
 typedef struct {
     int32_t N, hadamard, smooth_v, p_mode;
     float sm_scale, beta;
-    int32_t qk_fmt;  /* OR_QK_INT8 or OR_QK_MXFP4 */
+    int32_t qk_fmt;  /* OR_QK_INT8, OR_QK_FP8 or OR_QK_MXFP4 */
 } or_attn_cfg;
 
 /* Score scale in log2 units for one (query block, key block) pair:
@@ -522,6 +548,14 @@ static void attn_row(const or_attn_cfg *cfg, int i, const int8_t *qc, const floa
             float v;
             if (mx) {
                 v = (float)or_mx_score(&qm[(size_t)i * D], &qms[(size_t)i * 4], &km[key * D], &kms[key * 4]);
+            } else if (cfg->qk_fmt == OR_QK_FP8) {
+                /* FP8 (READING): the exact dot product of the decoded E4M3 codes (exact in fp64:
+                 * every product has 8 significant bits within a span of 2^-18 .. 2^17) rounded
+                 * once to fp32; a = fl(fl(s_q s_k) kappa) as for INT8 */
+                const uint8_t *qb = (const uint8_t *)q, *kb = (const uint8_t *)&kc[key * D];
+                double dot = 0.0;
+                for (int c = 0; c < D; ++c) dot += or_e4m3_decode(qb[c]) * or_e4m3_decode(kb[c]);
+                v = (float)dot;
             } else {
                 const int8_t *k = &kc[key * D];
                 int32_t dot = 0;

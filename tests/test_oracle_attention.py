@@ -44,15 +44,19 @@ def closed_form(pp, h, i, sm_scale, beta=-0.35):
     """Non-recurrent evaluation of the quantized pipeline for query row i of head h."""
     N = pp["N"]
     T = (N + 127) // 128
-    q = pp["q"].reshape(-1, T * 128, 128)[h, i].astype(np.int64)
+    q = pp["q"].reshape(-1, T * 128, 128)[h, i]
     sq = pp["q_scale"].reshape(-1, T)[h, i // 128]
-    kc = pp["k"].reshape(-1, T * 128, 128)[h, :N].astype(np.int64)
+    kc = pp["k"].reshape(-1, T * 128, 128)[h, :N]
     ks = pp["k_scale"].reshape(-1, T)[h]
     vd = _decode(pp["v"].reshape(-1, T * 128, 128)[h, :N])
     sv = pp["v_scale"].reshape(-1, 128)[h].astype(np.float64)
     mu = S.bits_to_f32(pp["v_mean"].reshape(-1, T, 128)[h]).astype(np.float64)
     kappa = np.float32(sm_scale * np.log2(np.e) / (128.0 if pp["hadamard"] else 1.0))
-    acc = kc @ q                                            # exact int64 dot products
+    if pp.get("qk_fmt", 0) == oracle.QK_FP8:
+        # E4M3 codes: exact fp64 dot products of the decoded values, rounded once to fp32
+        acc = (_decode(kc) @ _decode(q)).astype(np.float32)
+    else:
+        acc = kc.astype(np.int64) @ q.astype(np.int64)      # exact int64 dot products
     a = np.array([np.float32(np.float32(sq * ks[j]) * kappa) for j in range(T)], np.float32)
     tmax = np.array([np.float32(np.float32(acc[128 * j:128 * (j + 1)].max()) * a[j]) for j in range(T)], np.float32)
     m = np.maximum.accumulate(tmax)                         # running maximum after each tile
