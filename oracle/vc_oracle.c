@@ -319,7 +319,9 @@ static void quant_block_mx(const float *x, int valid, uint8_t *codes, uint8_t *s
  * OCP E4M3 codes per 128-row block, like the INT8 quantizer with 448 (the largest finite E4M3
  * value) in place of 127: scale = amax / 448, code = E4M3 nearest-even encoding of
  * fl(x * fl(448 / amax)) (at most 448 up to one rounding, so the encoder's saturation decides
- * nothing); all-zero block: scale 1, codes 0; padded rows: code 0. */
+ * nothing), with every code of zero magnitude stored as +0 (READING: the sign of an exact zero
+ * after the rotation depends on the order of its additions, which the method does not fix);
+ * all-zero block: scale 1, codes 0; padded rows: code 0. */
 static void quant_block_f8(const float *x, int valid, uint8_t *codes, float *scale)
 {
     float amax = 0.0f;
@@ -333,7 +335,10 @@ static void quant_block_f8(const float *x, int valid, uint8_t *codes, float *sca
     float inv = 448.0f / amax;
     *scale = amax / 448.0f;
     for (int r = 0; r < valid; ++r)
-        for (int c = 0; c < D; ++c) codes[r * D + c] = or_e4m3_encode(x[r * D + c] * inv);
+        for (int c = 0; c < D; ++c) {
+            uint8_t b = or_e4m3_encode(x[r * D + c] * inv);
+            codes[r * D + c] = (b & 0x7f) ? b : 0;
+        }
 }
 
 /* The score of one query row against one key row from their MX codes, exact (fp64):

@@ -20,7 +20,8 @@ def _rows_by_block(x):
 
 def test_prep_fp8_codes_are_the_library_cast_of_the_scaled_rotated_rows():
     """codes = torch's float8_e4m3fn cast (round to nearest even) of fl(x * fl(448 / amax)) per
-    128-row block of the rows prep rotates; scale = amax / 448; padded rows 0."""
+    128-row block of the rows prep rotates, zero magnitudes as +0; scale = amax / 448; padded
+    rows 0."""
     Q, K, V = S.make_qkv("tiny")
     w = S.WORKLOADS["tiny"]
     perm = S.random_perm(w.N, 4, w.B, w.H)
@@ -36,7 +37,8 @@ def test_prep_fp8_codes_are_the_library_cast_of_the_scaled_rotated_rows():
                 amax = np.float32(np.abs(x[j]).max())
                 inv = np.float32(np.float32(448.0) / amax)
                 assert scale[j] == np.float32(amax / np.float32(448.0))
-                want = torch.from_numpy(x[j] * inv).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+                want = torch.from_numpy(x[j] * inv).to(torch.float8_e4m3fn).view(torch.uint8).numpy().copy()
+                want[(want & 0x7F) == 0] = 0      # zero magnitudes stored as +0
                 assert np.array_equal(_rows_by_block(codes)[j], want), (h, j)
     # V operands do not depend on the Q/K format
     for key in ("v", "v_scale", "v_mean", "k_mean"):
@@ -45,12 +47,15 @@ def test_prep_fp8_codes_are_the_library_cast_of_the_scaled_rotated_rows():
 
 def test_fp8_quantizer_error_bound_and_extremes():
     """|code * scale - x| <= half an E4M3 spacing at |x| / scale (+ fp32 rounding of the scaled
-    value); the block maximum maps to +-448; a zero block gets scale 1 and zero codes; padded
-    rows of a ragged block are zero."""
+    value); the block maximum maps to +-448; a zero block gets scale 1 and zero codes; negative
+    zeros and negative values below half the smallest step are stored as +0; padded rows of a
+    ragged block are zero."""
     rng = np.random.default_rng(5)
     N = 300   # blocks of 128, 128, 44 rows
     Q = S.bf16_bits((rng.standard_normal((1, 1, N, 128)) * np.exp2(rng.integers(-8, 8, (1, 1, N, 1)))).astype(np.float32))
     Q[0, 0, 128:256] = 0
+    Q[0, 0, 5, :4] = 0x8000                                              # negative zeros
+    Q[0, 0, 6, 0] = S.bf16_bits(np.float32(-2.0 ** -60))                  # rounds to zero magnitude
     K = S.bf16_bits(rng.standard_normal((1, 1, N, 128)).astype(np.float32))
     V = S.bf16_bits(rng.standard_normal((1, 1, N, 128)).astype(np.float32))
     pf = oracle.prep(Q, K, V, (1, 1, N), rope=False, hadamard=False, smooth_k=False, qk_fmt=oracle.QK_FP8)
@@ -58,6 +63,7 @@ def test_fp8_quantizer_error_bound_and_extremes():
     dec = oracle.e4m3_decode(pf["q"][0, 0]).astype(np.float64)
     sc = pf["q_scale"][0, 0].astype(np.float64)
     assert sc[1] == 1.0 and not pf["q"][0, 0, 128:256].any()
+    assert not pf["q"][0, 0, 5, :4].any() and pf["q"][0, 0, 6, 0] == 0   # zero magnitudes are +0
     assert not pf["q"][0, 0, N:].any()
     for j, rows in ((0, slice(0, 128)), (2, slice(256, N))):
         xs = x[rows] / sc[j]
