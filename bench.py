@@ -16,7 +16,10 @@ Beside the main line: `loop_slice`, the denoising-loop slice (8 calls of the sam
 interpolated inputs, grouping on calls 0 and 4) with prep GB/s, attention TOPS and the amortized
 grouping share; `large_layer`, the 75600-token 40-head layer timed stage by stage; `mx4_layer`,
 the 4-bit variant (MXFP4 Q/K, FP8 P/V) on the 32760-token 40-head layer beside the 8-bit path on the
-same inputs and permutation, timed, and (with the CPU leg) both compared with exact fp64 attention.
+same inputs and permutation, timed, and (with the CPU leg) both compared with exact fp64 attention;
+`modes`, the score format (INT8 or FP8 Q/K) crossed with the probability path (ExpCast-FP8 or
+exponentiate-then-cast) on the main layer and its permutation, attention timed per mode and (with
+the CPU leg) compared with exact fp64 attention.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra] [--mx4-only]
 """
@@ -223,6 +226,45 @@ def mx4_layer(vc, S, reps=5):
     return res, (Qh, Kh, Vh, w.grid, heads, rows, samples)
 
 
+def modes_block(vc, S, Qd, Kd, Vd, perm, reps=10):
+    """The score format (INT8 / FP8 Q and K) crossed with the probability path (ExpCast-FP8 /
+    exponentiate-then-cast) on the main layer with its permutation: attention time per mode, and
+    the GPU outputs of a few heads on sampled rows for the accuracy comparison."""
+    import torch
+    w = S.WORKLOADS[WORKLOAD]
+    B, H, N = w.B, w.H, w.N
+    O = torch.empty((B, H, N, 128), dtype=torch.int16, device="cuda")
+    heads = [0, 5, 11]
+    T = (N + 127) // 128
+    rows = np.concatenate([np.arange(128 * b, min(N, 128 * b + 128)) for b in (0, T // 2, T - 1)]).astype(np.int32)
+    ops = 4.0 * B * H * N * N * 128
+    res, samples = {"sample_heads": heads, "sample_rows": int(rows.size)}, {}
+    for fmt, ftag in ((vc.QK_INT8, "int8"), (vc.QK_FP8, "fp8")):
+        for pm, ptag in ((vc.P_EXPCAST, "expcast"), (vc.P_EXP_THEN_CAST, "exp_then_cast")):
+            A = vc.Attention(B, H, w.grid, vc.make_opts(qk_fmt=fmt, p_mode=pm))
+            A.perm.copy_(perm)
+            A.prep(Qd, Kd, Vd)
+            fns = [lambda: A.forward(O)]
+            time_stages(fns, 3)
+            (t_attn,) = time_stages(fns, reps)
+            tops = ops / (t_attn * 1e-3) / 1e12
+            tag = f"{ftag}_{ptag}"
+            res[tag] = {"attn_ms": t_attn, "attention_tops": tops, "attention_frac_8bit_peak": tops / PEAK_8BIT_TOPS}
+            o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(B * H, N, 128)
+            samples[tag] = o[heads][:, rows].astype(np.float64)
+    return res, (heads, rows, samples)
+
+
+def modes_accuracy(Q, K, V, grid, sample):
+    """rel-L2 and PSNR of each mode's GPU output against exact fp64 attention (oracle)."""
+    import oracle
+    heads, rows, samples = sample
+    exact = oracle.reference_attention(Q[:, heads], K[:, heads], V[:, heads], grid, rows)
+    return {tag: {"rel_l2_vs_fp64": float(np.linalg.norm(o - exact) / np.linalg.norm(exact)),
+                  "psnr_vs_fp64_db": float(10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2)))}
+            for tag, o in samples.items()}
+
+
 def mx4_accuracy(sample):
     """rel-L2 and PSNR of both formats' GPU outputs against exact fp64 attention (oracle) on the
     sampled rows."""
@@ -343,6 +385,8 @@ def main():
         "wall_s_timed": wall,
     }
     if not args.no_extra:
+        print("[bench] score formats x probability paths", file=sys.stderr, flush=True)
+        out["modes"], modes_sample = modes_block(vc, S, Qd, Kd, Vd, A.perm.clone())
         print("[bench] denoising-loop slice", file=sys.stderr, flush=True)
         out["loop_slice"] = loop_slice(vc, S)
         print("[bench] large layer", file=sys.stderr, flush=True)
@@ -356,6 +400,9 @@ def main():
         out["cpu_baseline"] = r["baseline"]
         out["parity"] = r["parity"]
         if not args.no_extra:
+            print("[bench] score formats x probability paths: accuracy against fp64", file=sys.stderr, flush=True)
+            for tag, acc in modes_accuracy(Q, K, V, grid, modes_sample).items():
+                out["modes"][tag].update(acc)
             print("[bench] 4-bit variant accuracy against fp64", file=sys.stderr, flush=True)
             for tag, acc in mx4_accuracy(mx4_sample).items():
                 out["mx4_layer"][tag].update(acc)

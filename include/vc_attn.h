@@ -61,11 +61,15 @@ typedef struct {
 } vc_shape;
 
 enum { VC_QK_INT8 = 0,      /* per-128-row-block symmetric INT8 Q and K */
+       VC_QK_FP8 = 1,       /* per-128-row-block symmetric OCP E4M3 Q and K (Sec. 4.5) */
        VC_QK_MXFP4 = 2 };   /* OCP MX FP4 (E2M1) Q and K, one E8M0 scale per 32 channels of a row */
 enum { VC_P_EXPCAST = 0, VC_P_EXP_THEN_CAST = 1 };
 
 /* Options of the low-bit path.
- *   qk_fmt   : VC_QK_INT8 (the method's 8-bit path) or VC_QK_MXFP4 (the 4-bit variant: Q and K
+ *   qk_fmt   : VC_QK_INT8 (the method's 8-bit path), VC_QK_FP8 (Q and K as E4M3 codes per 128-row
+ *              block, scale amax/448, nearest-even, codes of zero magnitude stored as +0: the
+ *              configuration of Sec. 4.5 for matrix units without INT8; the scores come out of
+ *              the FP8 matrix product in fp32) or VC_QK_MXFP4 (the 4-bit variant: Q and K
  *              quantized after the Hadamard rotation by 32-channel blocks, shared exponent
  *              floor(log2(amax)) - 2, elements rounded to the nearest E2M1 value with ties to the
  *              even code and saturation at 6; the scores come out of the scaled FP4 matrix
@@ -117,6 +121,13 @@ typedef struct {
  *          ((rb*4 + dc)*2 + dh)*512 + r*16 + e. q rows are in query order (q_perm order when a
  *          q_perm is given); k rows in permuted order K' = K[perm]. Padded rows hold 0.
  *   q_scale, k_scale : fp32 [B, H, T], one scale per 128-row block (code * scale = value).
+ *   With qk_fmt = VC_QK_FP8 instead:
+ *   q, k : E4M3 bytes, B*H*Np*128 bytes. Per (b, h) and 128-row block j, the 16384 bytes are
+ *          ordered [rb 4][m 2][h 2][half 2][r 32][e 16]: byte (row, ch) sits at
+ *          ((((rb*2 + m)*2 + h)*2 + half)*32 + r)*16 + e with rb = row/32, r = row%32, m = ch/64,
+ *          h = (ch%64)/32, half = (ch%32)/16, e = ch%16 (lane h*32 + r of the FP8 32x32x64
+ *          product holds channels 64m + 32h .. + 31 of one row as two 16-byte halves).
+ *          q_scale, k_scale as for INT8 (amax/448).
  *   With qk_fmt = VC_QK_MXFP4 instead:
  *   q, k : packed E2M1 codes, B*H*Np*64 bytes. Per (b, h) and 128-row block j, the 8192 bytes are
  *          ordered [rb 4][m 2][h 2][r 32][16 bytes]: channel ch of row `row` is the nibble

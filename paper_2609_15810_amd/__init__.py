@@ -21,7 +21,7 @@ VC_OK = 0
 STATUS = {0: "VC_OK", 1: "VC_ERR_NULL", 2: "VC_ERR_SHAPE", 3: "VC_ERR_UNSUPPORTED", 4: "VC_ERR_WORKSPACE",
           5: "VC_ERR_ALIGN", 6: "VC_ERR_HIP", 7: "VC_ERR_INTERNAL"}
 P_EXPCAST, P_EXP_THEN_CAST = 0, 1
-QK_INT8, QK_MXFP4 = 0, 2
+QK_INT8, QK_FP8, QK_MXFP4 = 0, 1, 2
 GROUP_IDENTITY, GROUP_CUBE, GROUP_KMEANS = 0, 1, 2
 
 
@@ -161,8 +161,8 @@ class PreppedBuffers:
 
 
 def alloc_prepped(shape: Shape, device="cuda", qk_fmt: int = None) -> PreppedBuffers:
-    """Buffers for vc_attn_prep / vc_attn_forward. INT8: q, k int8 [B, H, Np, 128] and fp32 block
-    scales; MXFP4: q, k packed codes [B, H, Np, 64] bytes and E8M0 scale bytes [B, H, Np, 4]."""
+    """Buffers for vc_attn_prep / vc_attn_forward. INT8 and FP8: q, k [B, H, Np, 128] bytes and fp32
+    block scales; MXFP4: q, k packed codes [B, H, Np, 64] bytes and E8M0 scale bytes [B, H, Np, 4]."""
     import torch
     B, H, N = shape.B, shape.H, shape.N
     T = (N + 127) // 128

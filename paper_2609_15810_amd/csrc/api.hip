@@ -29,7 +29,7 @@ vc_status check_shape(const vc_shape* s) {
 
 vc_status check_opts(const vc_opts* o) {
   if (!o) return VC_ERR_NULL;
-  if (o->qk_fmt != VC_QK_INT8 && o->qk_fmt != VC_QK_MXFP4) return VC_ERR_UNSUPPORTED;
+  if (o->qk_fmt != VC_QK_INT8 && o->qk_fmt != VC_QK_FP8 && o->qk_fmt != VC_QK_MXFP4) return VC_ERR_UNSUPPORTED;
   if (o->p_mode != VC_P_EXPCAST && o->p_mode != VC_P_EXP_THEN_CAST) return VC_ERR_UNSUPPORTED;
   const int32_t flags[4] = {o->rope, o->hadamard, o->smooth_k, o->smooth_v};
   for (int32_t f : flags)

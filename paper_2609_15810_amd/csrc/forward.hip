@@ -38,6 +38,9 @@
 // statically. Tiles are visited in ascending order with the running maximum updated once per
 // 128-key tile, the schedule on which the codes are defined.
 //
+// FP8 Q/K variant (E4M3 per 128-row block, for matrix units without INT8): the scores come from
+// two FP8 32x32x64 products per 32-key block (each lane 32 channels of its row), already fp32.
+//
 // 4-bit variant (OCP MXFP4 Q and K): the scores come from the scaled FP4 product
 // v_mfma_scale_f32_32x32x64_f8f6f4 (two per 32-key block), each lane's E8M0 byte scaling its
 // 32-channel block, so S^T arrives in fp32 with the block scales applied and the score scale of
@@ -180,9 +183,11 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
-template <int PMODE, bool MX>
+template <int PMODE, int QKF>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_fwd(FwdArgs a) {
-  using SV = std::conditional_t<MX, v16f, v16i>;  // a lane's 16 scores of one 32-key block
+  constexpr bool I8 = QKF == VC_QK_INT8, F8 = QKF == VC_QK_FP8, MX = QKF == VC_QK_MXFP4;
+  using SV = std::conditional_t<I8, v16i, v16f>;  // a lane's 16 scores of one 32-key block
+  using QO = std::conditional_t<F8, v8i, v4i>;    // one Q or K operand of the score product
   // K_t in kb[t % 4] (MXFP4: codes, then scale bytes at MX_CODE_BYTES); V_t with its 128 bf16 block means in vb[t % 4]; mu_t / s_V as bf16 hi + lo
   // in slot t % 8 of ub[(t / 8) % 2]; (r_t, m_t) per query in slot t % 8 of rm[wave]
   __shared__ __attribute__((aligned(16))) uint8_t kb0[TILE_BYTES];
@@ -207,12 +212,23 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   const int gq = NW * qt + wave;  // global 32-query group
   const int qblock = min(gq >> 2, T - 1);
   const int qrb = gq & 3;         // the group's 32-row block within its 128-row block
-  // INT8: four 32-channel operands, scale sq per 128-row block; MXFP4: two 64-channel operands
-  // (each lane one 32-channel block of its query) with their E8M0 bytes qsc[m]
-  v4i qop[MX ? 2 : 4];
+  // INT8: four 32-channel operands, scale sq per 128-row block; FP8: two 64-channel operands (a
+  // lane holds 32 channels of its query), scale sq; MXFP4: two 64-channel operands with the E8M0
+  // bytes qsc[m] of the lane's 32-channel blocks
+  QO qop[I8 ? 4 : 2];
   float sq = 1.f;
   int qsc[2] = {0, 0};
-  if constexpr (MX) {
+  if constexpr (F8) {
+    const uint8_t* qblk = reinterpret_cast<const uint8_t*>(a.q) + (tile0 + qblock) * TILE_BYTES;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const uint8_t* p = qblk + ((((qrb * 2 + m) * 2 + kh) * 2) * 32 + col) * 16;
+      const u4 lo = *reinterpret_cast<const u4*>(p);
+      const u4 hi = *reinterpret_cast<const u4*>(p + 512);
+      qop[m] = v8i{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+    sq = a.q_scale[tile0 + qblock];
+  } else if constexpr (MX) {
     const uint8_t* qblk = reinterpret_cast<const uint8_t*>(a.q) + (tile0 + qblock) * MX_CODE_BYTES;
 #pragma unroll
     for (int m = 0; m < 2; ++m)
@@ -354,6 +370,16 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   auto mx_scales = [&](const uint8_t* kt) __attribute__((always_inline)) -> uint2 {
     return *reinterpret_cast<const uint2*>(kt + MX_CODE_BYTES + lane * 8);
   };
+  // FP8 key operands of block kb: 32 bytes per lane as two 16-byte halves 512 bytes apart
+  auto f8_kops = [&](int kb, const uint8_t* kt, v8i (&k)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const uint8_t* p = kt + ((((kb * 2 + m) * 2 + kh) * 2) * 32 + col) * 16;
+      const u4 lo = *reinterpret_cast<const u4*>(p);
+      const u4 hi = *reinterpret_cast<const u4*>(p + 512);
+      k[m] = v8i{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+  };
 
   // scores of tile t (K_t in kt) into s
   auto qk = [&](auto MASKC, int t, const uint8_t* kt) __attribute__((always_inline)) {
@@ -368,6 +394,16 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
       s[2] = qk_mx(std::integral_constant<int, 2>{}, kops, (int)ksw.y);
       mx_kops(3, kt, kops);
       s[3] = qk_mx(std::integral_constant<int, 3>{}, kops, (int)ksw.y);
+    } else if constexpr (F8) {
+      ksc = kscale[t];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        v8i kops[2];
+        f8_kops(kb, kt, kops);
+        v16f acc = {};
+        acc = mfma_f8(kops[0], qop[0], acc);
+        s[kb] = mfma_f8(kops[1], qop[1], acc);
+      }
     } else {
       ksc = kscale[t];
 #pragma unroll
@@ -386,7 +422,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 
   // running maximum of tile t (scores in s) into m_new, alpha, codes into pn
   auto softmax = [&](auto LASTC, int t, v8i (&pn)[2], float& alpha, float& m_new) __attribute__((always_inline)) {
-    // score scale a = fl(fl(s_q s_k) kappa) (INT8) or kappa (MXFP4: the block scales are inside s)
+    // score scale a = fl(fl(s_q s_k) kappa) (INT8, FP8) or kappa (MXFP4: the block scales are in s)
     const float a_s = MX ? a.kappa : (sq * ksc) * a.kappa;
     using E = std::remove_reference_t<decltype(s[0][0])>;
     E mk[4];
@@ -506,23 +542,29 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
       for (int r = 2; r < 16; r += 2) m = smax3(m, s[kb][r], s[kb][r + 1]);
       return m;
     };
-    // key operands of block kb (INT8: 4 x 32 channels; MXFP4: 2 x 64 channels and, with block 0,
-    // the lane's two scale dwords of the tile)
-    constexpr int NKOP = MX ? 2 : 4;
+    // key operands of block kb (INT8: 4 x 32 channels; FP8: 2 x 64 channels; MXFP4: 2 x 64
+    // channels and, with block 0, the lane's two scale dwords of the tile)
+    constexpr int NKOP = I8 ? 4 : 2;
     uint2 ksw = {0u, 0u};
-    auto load_kops = [&](int kb, v4i (&k)[NKOP]) __attribute__((always_inline)) {
+    auto load_kops = [&](int kb, QO (&k)[NKOP]) __attribute__((always_inline)) {
       if constexpr (MX) {
         if (kb == 0) ksw = mx_scales(kt);
         mx_kops(kb, kt, k);
+      } else if constexpr (F8) {
+        f8_kops(kb, kt, k);
       } else {
 #pragma unroll
         for (int dc = 0; dc < 4; ++dc) k[dc] = *reinterpret_cast<const v4i*>(kt + ((kb * 4 + dc) * 2 + kh) * 512 + col * 16);
       }
     };
-    auto qk_kb = [&](auto KBC, const v4i (&k)[NKOP]) __attribute__((always_inline)) {
+    auto qk_kb = [&](auto KBC, const QO (&k)[NKOP]) __attribute__((always_inline)) {
       constexpr int kb = decltype(KBC)::value;
       if constexpr (MX) {
         s[kb] = qk_mx(KBC, k, kb < 2 ? (int)ksw.x : (int)ksw.y);
+      } else if constexpr (F8) {
+        v16f acc = {};
+        acc = mfma_f8(k[0], qop[0], acc);
+        s[kb] = mfma_f8(k[1], qop[1], acc);
       } else {
         v16i acc = {};
 #pragma unroll
@@ -554,7 +596,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     };
     // at most 32 registers of operands staged at any time
     v8i va[2], vb[2];
-    v4i k0[NKOP], k1[NKOP];
+    QO k0[NKOP], k1[NKOP];
     // R0: value operands 0, 1
     va[0] = load_vop(vt, 0);
     va[1] = load_vop(vt, 1);
@@ -575,7 +617,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     o[3] = mfma_f8(vb[1], pc[0], o[3]);
     va[0] = load_vop(vt, 4);
     va[1] = load_vop(vt, 5);
-    a_s = MX ? a.kappa : (sq * ksc) * a.kappa;  // fl(fl(s_q s_k) kappa) for INT8
+    a_s = MX ? a.kappa : (sq * ksc) * a.kappa;  // fl(fl(s_q s_k) kappa) for INT8 and FP8
     E mx = smax(smax(mk0, mk1), smax(kmax(2), kmax(3)));
     mx = half_max(mx);
     m_new = fmaxf(m_run, (float)mx * a_s);
@@ -726,14 +768,14 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s) {
   const dim3 grid((a.N + NQ - 1) / NQ, BH);
-  const bool mx = a.qk_fmt == VC_QK_MXFP4;
-  if (a.p_mode == 0) {
-    if (mx) attn_fwd<0, true><<<grid, NTH, 0, s>>>(a);
-    else attn_fwd<0, false><<<grid, NTH, 0, s>>>(a);
-  } else {
-    if (mx) attn_fwd<1, true><<<grid, NTH, 0, s>>>(a);
-    else attn_fwd<1, false><<<grid, NTH, 0, s>>>(a);
-  }
+  auto go = [&](auto PC) {
+    constexpr int pm = decltype(PC)::value;
+    if (a.qk_fmt == VC_QK_MXFP4) attn_fwd<pm, VC_QK_MXFP4><<<grid, NTH, 0, s>>>(a);
+    else if (a.qk_fmt == VC_QK_FP8) attn_fwd<pm, VC_QK_FP8><<<grid, NTH, 0, s>>>(a);
+    else attn_fwd<pm, VC_QK_INT8><<<grid, NTH, 0, s>>>(a);
+  };
+  if (a.p_mode == 0) go(std::integral_constant<int, 0>{});
+  else go(std::integral_constant<int, 1>{});
   return hipGetLastError();
 }
 

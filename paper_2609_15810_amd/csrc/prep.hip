@@ -7,9 +7,9 @@
 //                 rows of original-order block j summed per channel (the centering statistics).
 //   prep_finalize grid (B*H, 16), 256 threads: key channel mean and per-channel value scale.
 //   prep_quant    grid (T, B*H, 3), 256 threads. z = 0: K' rows (gather, RoPE, centering,
-//                 Hadamard, per-block INT8 or MXFP4); z = 1: V' rows (gather, demean, per-channel
-//                 E4M3), transposed into the tile order of the attention kernel; z = 2: Q rows
-//                 (RoPE, Hadamard, per-block INT8 or MXFP4).
+//                 Hadamard, per-block INT8 or E4M3, or MXFP4); z = 1: V' rows (gather, demean,
+//                 per-channel E4M3), transposed into the tile order of the attention kernel;
+//                 z = 2: Q rows (RoPE, Hadamard, per-block INT8 or E4M3, or MXFP4).
 // All floating-point steps that decide a stored code are written as single IEEE fp32
 // operations in a fixed order (compiled with -ffp-contract=off; fused multiply-adds are spelled
 // out), so the codes, scales and means are reproducible bit for bit.
@@ -473,9 +473,11 @@ __device__ __forceinline__ uint32_t fp4_code(float v) {
 }
 
 // Q (IS_K = false) or K' (IS_K = true) rows of block j: gather, RoPE, centering (K), Hadamard,
-// then either per-block symmetric INT8 (scale = amax/127, code = rint(x * (127/amax))) or, with
-// MX, MXFP4 by 32-channel blocks (E8M0 scale byte floor(log2(amax)) - 2 + 127 per block).
-template <bool IS_K, bool ROPE, bool HAD, bool MX>
+// then, by the format QF: per-block symmetric INT8 (VC_QK_INT8: scale = amax/127, code =
+// rint(x * (127/amax))), per-block symmetric E4M3 (VC_QK_FP8: scale = amax/448, code = the
+// nearest-even E4M3 of x * (448/amax), +0 for codes of zero magnitude) or MXFP4 by 32-channel
+// blocks (VC_QK_MXFP4: E8M0 scale byte floor(log2(amax)) - 2 + 127 per block).
+template <bool IS_K, bool ROPE, bool HAD, int QF>
 __device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red, uint8_t* stage) {
   const int j = blockIdx.x, bh = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, k4 = lane & 3;
@@ -514,7 +516,7 @@ __device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red, uint8_t*
   }
 
   const float sigma = HAD ? (((k4 ^ (k4 >> 1)) & 1) ? -1.f : 1.f) : 1.f;
-  if constexpr (MX) {
+  if constexpr (QF == VC_QK_MXFP4) {
     // channels 32 i .. 32 i + 31 of a row (one MX block) sit in the 4 lanes of the row's quad,
     // 8 each; lane (h*32 + r) of the scaled product's operand = row r, block 2m + h
     uint8_t* codes = reinterpret_cast<uint8_t*>(IS_K ? a.k : a.q) + ((size_t)bh * a.T + j) * (BLK * D / 2);
@@ -558,8 +560,37 @@ __device__ __forceinline__ void quant_qk(const PrepArgs& a, float* red, uint8_t*
   if (lane == 0) red[wave] = m;
   __syncthreads();
   const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  const float inv = amax > 0.f ? 127.f / amax : 0.f;
-  if (threadIdx.x == 0) (IS_K ? a.k_scale : a.q_scale)[(size_t)bh * a.T + j] = amax > 0.f ? amax / 127.f : 1.f;
+  constexpr float top = QF == VC_QK_FP8 ? 448.f : 127.f;  // the largest code value
+  const float inv = amax > 0.f ? top / amax : 0.f;
+  if (threadIdx.x == 0) (IS_K ? a.k_scale : a.q_scale)[(size_t)bh * a.T + j] = amax > 0.f ? amax / top : 1.f;
+  if constexpr (QF == VC_QK_FP8) {
+    // x * (s inv) = s * fl(x inv) exactly, and E4M3 rounding is symmetric, so the carried
+    // Hadamard sign goes into the multiplier; |fl(x inv)| <= 448 (1 + 2^-24)^2 converts to at most
+    // 448. Lane k4 holds channels 8 k4 .. 8 k4 + 7 of each 32-channel block i = 2m + h: bytes
+    // 8 (k4 & 1) .. of half k4 / 2 of the 32 bytes that lane (h*32 + r) of the FP8 product holds.
+    const float mult = sigma * inv;
+    uint8_t* codes = reinterpret_cast<uint8_t*>(IS_K ? a.k : a.q) + ((size_t)bh * a.T + j) * (BLK * D);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int rl = wave * 32 + it * 16 + (lane >> 2), rb = rl >> 5, r = rl & 31;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t w[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float* y = &x[it][i][4 * u];
+          uint32_t v = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[0] * mult, y[1] * mult, 0, false);
+          v = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[2] * mult, y[3] * mult, (int)v, true);
+          // +0 for every code of zero magnitude (a zero's sign depends on the butterfly order)
+          const uint32_t t = v & 0x7f7f7f7fu;
+          w[u] = v & (((t + 0x7f7f7f7fu) & 0x80808080u) | 0x7f7f7f7fu);
+        }
+        const int off = ((((rb * 2 + (i >> 1)) * 2 + (i & 1)) * 2 + (k4 >> 1)) * 32 + r) * 16 + 8 * (k4 & 1);
+        *reinterpret_cast<uint2*>(codes + off) = make_uint2(w[0], w[1]);
+      }
+    }
+    return;
+  }
   // the lane's sign from the cross-lane butterflies goes into the multiplier: x * (s inv) is
   // exactly s * fl(x inv). |fl(x inv)| <= 127 (1 + 2^-24)^2 < 127.5, so adding 1.5 * 2^23 rounds
   // it to the nearest integer, ties to even (the oracle's rint; its clamp to +-127 never acts),
@@ -637,18 +668,18 @@ __device__ __forceinline__ void quant_v(const PrepArgs& a, uint8_t (*vt)[D + 8])
 }
 
 // grid (T, B*H, 3): z = 0 K' rows, z = 1 V' rows, z = 2 Q rows of block blockIdx.x.
-template <bool ROPE, bool HAD, bool MX>
+template <bool ROPE, bool HAD, int QF>
 __global__ __launch_bounds__(256) void prep_quant(PrepArgs a) {
   __shared__ float red[4];
   // V codes of the block, row-major (8-byte rows), for the transpose; MX scale bytes of a Q/K block
   __shared__ uint8_t vt[BLK][D + 8];
   // K' and V' first: their rows were just read by the statistics pass and may still be cached
   if (blockIdx.z == 0)
-    quant_qk<true, ROPE, HAD, MX>(a, red, &vt[0][0]);
+    quant_qk<true, ROPE, HAD, QF>(a, red, &vt[0][0]);
   else if (blockIdx.z == 1)
     quant_v(a, vt);
   else
-    quant_qk<false, ROPE, HAD, MX>(a, red, &vt[0][0]);
+    quant_qk<false, ROPE, HAD, QF>(a, red, &vt[0][0]);
 }
 
 hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
@@ -659,24 +690,26 @@ hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s) {
     prep_stats<false><<<sgrid, 64, 0, s>>>(a);
   prep_finalize<<<dim3(BH, 16), 256, 0, s>>>(a);
   const dim3 grid(a.T, BH, 3);
-  auto quant = [&](auto MXC) {
-    constexpr bool mx = decltype(MXC)::value;
+  auto quant = [&](auto QFC) {
+    constexpr int qf = decltype(QFC)::value;
     if (a.rope) {
       if (a.hadamard)
-        prep_quant<true, true, mx><<<grid, 256, 0, s>>>(a);
+        prep_quant<true, true, qf><<<grid, 256, 0, s>>>(a);
       else
-        prep_quant<true, false, mx><<<grid, 256, 0, s>>>(a);
+        prep_quant<true, false, qf><<<grid, 256, 0, s>>>(a);
     } else {
       if (a.hadamard)
-        prep_quant<false, true, mx><<<grid, 256, 0, s>>>(a);
+        prep_quant<false, true, qf><<<grid, 256, 0, s>>>(a);
       else
-        prep_quant<false, false, mx><<<grid, 256, 0, s>>>(a);
+        prep_quant<false, false, qf><<<grid, 256, 0, s>>>(a);
     }
   };
   if (a.qk_fmt == VC_QK_MXFP4)
-    quant(std::integral_constant<bool, true>{});
+    quant(std::integral_constant<int, VC_QK_MXFP4>{});
+  else if (a.qk_fmt == VC_QK_FP8)
+    quant(std::integral_constant<int, VC_QK_FP8>{});
   else
-    quant(std::integral_constant<bool, false>{});
+    quant(std::integral_constant<int, VC_QK_INT8>{});
   return hipGetLastError();
 }
 

@@ -73,3 +73,19 @@ def untile_mx_scales(phys: np.ndarray) -> np.ndarray:
     shp = phys.shape
     blocks = phys.reshape(-1, 128 * 4).astype(np.uint8)
     return blocks[:, MX_SCALE_INDEX.reshape(-1)].reshape(shp)
+
+
+def _f8_index():
+    """FP8 Q/K block layout [rb 4][m 2][h 2][half 2][r 32][e 16]: lane h*32 + r of the FP8
+    32x32x64 product holds channels 64m + 32h .. + 31 of row 32rb + r as two 16-byte halves."""
+    row = np.arange(128)[:, None]
+    ch = np.arange(128)[None, :]
+    rb, r, m, h, half, e = row // 32, row % 32, ch // 64, (ch % 64) // 32, (ch % 32) // 16, ch % 16
+    return ((((rb * 2 + m) * 2 + h) * 2 + half) * 32 + r) * 16 + e
+
+
+F8_INDEX = _f8_index()
+
+
+def untile_f8(phys):
+    return untile(phys, F8_INDEX)

@@ -65,7 +65,7 @@ def test_prep_validation(L):
     assert prep_call(L, shape(), bad) == 3
     bad = vc.make_opts(); bad.smooth_v = 2
     assert prep_call(L, shape(), bad) == 3
-    bad = vc.make_opts(); bad.qk_fmt = 1
+    bad = vc.make_opts(); bad.qk_fmt = 3
     assert prep_call(L, shape(), bad) == 3
     assert prep_call(L, shape(), o, ws_bytes=16) == 4
     P = vc.Prepped(*([FAKE] * 8)); P.v_mean = None
