@@ -21,7 +21,10 @@ same inputs and permutation, timed, and (with the CPU leg) both compared with ex
 exponentiate-then-cast) on the main layer and its permutation, attention timed per mode and (with
 the CPU leg) compared with exact fp64 attention.
 
+`--grouping-study` runs only the token-order study instead (see `grouping_study`).
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra] [--mx4-only]
+                       [--grouping-study]
 """
 from __future__ import annotations
 
@@ -265,6 +268,170 @@ def modes_accuracy(Q, K, V, grid, sample):
             for tag, o in samples.items()}
 
 
+def _v_layout_index():
+    """Position of (key, channel) in a 128x128 block of the value codes (the tiled order the
+    library documents: [kc 2][db 4][kh 2][sh 2][c 32][t 16])."""
+    key = np.arange(128)[:, None]
+    ch = np.arange(128)[None, :]
+    kb, wk = key // 32, key % 32
+    kc, sh, kh, t = kb // 2, kb % 2, (wk % 8) // 4, 4 * (wk // 8) + wk % 4
+    return ((((kc * 4 + ch // 32) * 2 + kh) * 2 + sh) * 32 + ch % 32) * 16 + t
+
+
+def _e4m3_roundtrip(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def _bf16_round(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def _value_stats(Vh, perm, rot=None):
+    """Block demeaning + per-channel E4M3 of one head's values in the order `perm`, evaluated on the
+    host: (energy share the block means remove, relative squared error of the reconstruction).
+    rot: optional orthonormal channel rotation applied before quantizing and undone after."""
+    N = Vh.shape[0]
+    X = Vh[perm] @ rot if rot is not None else Vh[perm]
+    T = (N + 127) // 128
+    Xp = np.zeros((T * 128, 128))
+    Xp[:N] = X
+    cnt = np.minimum(128, N - 128 * np.arange(T)).astype(np.float64)
+    mu_exact = Xp.reshape(T, 128, 128).sum(axis=1) / cnt[:, None]
+    share = float((cnt * (mu_exact ** 2).sum(axis=1)).sum() / (X ** 2).sum())
+    mu = _bf16_round(mu_exact)
+    R = X - np.repeat(mu, 128, axis=0)[:N]
+    sv = np.abs(R).max(axis=0) / 448.0
+    sv[sv == 0] = 1.0
+    Xq = _e4m3_roundtrip(R / sv) * sv + np.repeat(mu, 128, axis=0)[:N]
+    if rot is not None:
+        Xq = Xq @ rot.T
+    return share, float(((Xq - Vh[perm]) ** 2).sum() / (Vh ** 2).sum())
+
+
+def _balanced_kmeans(Vh, init_perm, rounds=3):
+    """Clusters of exactly 128 tokens (the last one ragged): Lloyd rounds whose assignment step
+    fills clusters greedily, each pass giving every unassigned token to its nearest cluster with
+    room, nearest tokens first. Starts from the 128-token blocks of init_perm."""
+    N = Vh.shape[0]
+    T = (N + 127) // 128
+    cap0 = np.minimum(128, N - 128 * np.arange(T))
+    X = Vh.astype(np.float32)
+    C = np.stack([X[init_perm[128 * t:128 * t + cap0[t]]].mean(axis=0) for t in range(T)])
+    for _ in range(rounds):
+        d = (X ** 2).sum(1)[:, None] - 2 * X @ C.T + (C ** 2).sum(1)[None, :]
+        lab = np.full(N, -1)
+        cap = cap0.copy()
+        while (lab < 0).any():
+            todo = np.nonzero(lab < 0)[0]
+            dd = d[todo].copy()
+            dd[:, cap == 0] = np.inf
+            best = dd.argmin(axis=1)
+            bd = dd[np.arange(todo.size), best]
+            order = np.lexsort((bd, best))
+            tok, cl = todo[order], best[order]
+            first = np.r_[0, np.nonzero(np.diff(cl))[0] + 1]
+            rank = np.arange(cl.size) - np.repeat(first, np.diff(np.r_[first, cl.size]))
+            take = rank < cap[cl]
+            lab[tok[take]] = cl[take]
+            np.subtract.at(cap, cl[take], 1)
+        C = np.stack([X[lab == t].mean(axis=0) for t in range(T)])
+    return np.argsort(lab, kind="stable").astype(np.int64)
+
+
+def grouping_study(vc, S, n_host_heads=8, reps=5):
+    """Token order fed to the value quantizer, on the 40-head 32760-token layer at step 4 of the
+    denoising-loop interpolation (the warm start takes its centroids from step 3): the share of
+    block energy the means remove, the relative squared error of the demeaned per-channel E4M3
+    values, and the grouping time over the attention time of one call. GPU orders (sequence,
+    static cube, k-means cold / warm, k swept) are timed on the GPU; the orders not built there
+    (Hadamard rotation of V, balanced k-means) are evaluated on the host on the first heads."""
+    import torch
+    from scipy.linalg import hadamard
+    name = "dit_small_h40"
+    w = S.WORKLOADS[name]
+    B, H, N = w.B, w.H, w.N
+    print("[bench] grouping study: inputs", file=sys.stderr, flush=True)
+    prev, cur = S.make_interpolated(name, 3), S.make_interpolated(name, 4)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    Qd, Kd, Vd = (dev(x) for x in cur)
+    Vprev = dev(prev[2])
+    Vh = S.bits_to_f32(cur[2]).reshape(B * H, N, 128).astype(np.float64)
+    O = torch.empty((B, H, N, 128), dtype=torch.int16, device="cuda")
+    A0 = vc.Attention(B, H, w.grid, gopts=vc.make_group_opts(mode=vc.GROUP_IDENTITY))
+    A0.group(Vd)
+    A0.prep(Qd, Kd, Vd)
+    time_stages([lambda: A0.forward(O)], 2)
+    (t_attn,) = time_stages([lambda: A0.forward(O)], reps)
+
+    def evaluate(perm_all, heads):
+        sh, er = zip(*(_value_stats(Vh[h], perm_all[h]) for h in heads))
+        return float(np.mean(sh)), float(np.sum([e * (Vh[h] ** 2).sum() for h, e in zip(heads, er)]) /
+                                         np.sum([(Vh[h] ** 2).sum() for h in heads]))
+
+    rows, perms = [], {}
+    all_heads, host_heads = list(range(B * H)), list(range(min(n_host_heads, B * H)))
+
+    def gpu_row(label, gopts, warm_from=None):
+        A = vc.Attention(B, H, w.grid, gopts=gopts)
+        if warm_from is not None:
+            A.gopts = vc.make_group_opts(k=gopts.k, iters=8)
+            A.group(warm_from)
+            A.gopts = gopts
+        fns = [lambda: A.group(Vd)]
+        if warm_from is None:
+            time_stages(fns, 1)
+            (t,) = time_stages(fns, reps)
+        else:
+            # a warm start must begin from the previous step's centroids every time
+            cents = A.centroids.clone()
+            ts = []
+            for _ in range(reps):
+                A.centroids.copy_(cents)
+                ts.append(time_stages(fns, 1)[0])
+            t = float(np.mean(ts))
+        perm = A.perm.cpu().numpy().reshape(B * H, N).astype(np.int64)
+        perms[label] = perm
+        share, err = evaluate(perm, all_heads)
+        rows.append({"order": label, "energy_removed": share, "value_rel_sq_err": err,
+                     "group_ms": t, "overhead_pct_attn": 100.0 * t / t_attn, "heads": B * H, "where": "GPU"})
+        print(f"[bench]   {label}: share {share:.4f} err {err:.3e} {t:.3f} ms", file=sys.stderr, flush=True)
+
+    seq = np.tile(np.arange(N), (B * H, 1))
+    sh, er = evaluate(seq, all_heads)
+    rows.append({"order": "sequence", "energy_removed": sh, "value_rel_sq_err": er, "group_ms": 0.0,
+                 "overhead_pct_attn": 0.0, "heads": B * H, "where": "GPU (identity)"})
+    e_plain = np.sum([(((_e4m3_roundtrip(Vh[h] / (np.abs(Vh[h]).max(0) / 448)) * (np.abs(Vh[h]).max(0) / 448))
+                        - Vh[h]) ** 2).sum() for h in all_heads]) / np.sum([(Vh[h] ** 2).sum() for h in all_heads])
+    rows.append({"order": "sequence, no block demeaning", "energy_removed": 0.0, "value_rel_sq_err": float(e_plain),
+                 "group_ms": 0.0, "overhead_pct_attn": 0.0, "heads": B * H, "where": "host"})
+    gpu_row("static cube 4x2x16", vc.make_group_opts(mode=vc.GROUP_CUBE))
+    for k in (8, 16, 32, 64):
+        gpu_row(f"k-means k={k}, 8 rounds", vc.make_group_opts(k=k, iters=8))
+    gpu_row("k-means k=32, warm-started, 4 rounds", vc.make_group_opts(k=32, iters=4, warm_start=True),
+            warm_from=Vprev)
+    Hm = hadamard(128) / np.sqrt(128.0)
+    print("[bench]   host rows", file=sys.stderr, flush=True)
+    sh, er = zip(*(_value_stats(Vh[h], seq[h], rot=Hm) for h in host_heads))
+    wgt = [(Vh[h] ** 2).sum() for h in host_heads]
+    rows.append({"order": "Hadamard on V (sequence order)", "energy_removed": float(np.mean(sh)),
+                 "value_rel_sq_err": float(np.dot(er, wgt) / np.sum(wgt)), "group_ms": None,
+                 "overhead_pct_attn": None, "heads": len(host_heads), "where": "host"})
+    bal = {h: _balanced_kmeans(Vh[h], perms["k-means k=32, 8 rounds"][h]) for h in host_heads}
+    sh, er = zip(*(_value_stats(Vh[h], bal[h]) for h in host_heads))
+    rows.append({"order": "balanced k-means (128 tokens per cluster)", "energy_removed": float(np.mean(sh)),
+                 "value_rel_sq_err": float(np.dot(er, wgt) / np.sum(wgt)), "group_ms": None,
+                 "overhead_pct_attn": None, "heads": len(host_heads), "where": "host"})
+    # the GPU rows again on the host heads only, for a like-for-like comparison with the host rows
+    for r in list(rows):
+        if r["where"].startswith("GPU") and r["order"] != "sequence":
+            r["value_rel_sq_err_first_heads"] = evaluate(perms[r["order"]], host_heads)[1]
+    rows[0]["value_rel_sq_err_first_heads"] = evaluate(seq, host_heads)[1]
+    return {"workload": f"B={B} H={H} N={N} (grid {w.grid[0]}x{w.grid[1]}x{w.grid[2]}), denoising-loop step 4 of 8",
+            "attn_ms": t_attn, "host_heads": len(host_heads), "rows": rows}
+
+
 def mx4_accuracy(sample):
     """rel-L2 and PSNR of both formats' GPU outputs against exact fp64 attention (oracle) on the
     sampled rows."""
@@ -286,6 +453,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the denoising-loop slice and the large layer (reported beside the main line)")
+    ap.add_argument("--grouping-study", action="store_true",
+                    help="run only the token-order study (energy removed, value error, overhead) and print it")
     ap.add_argument("--mx4-only", action="store_true",
                     help="run only the 4-bit variant block (for kernel traces of that shape) and print it")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -304,6 +473,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.grouping_study:
+        print(json.dumps({"grouping_study": grouping_study(vc, S)}), flush=True)
+        return
     if args.mx4_only:
         res, _ = mx4_layer(vc, S, reps=args.steps)
         if args.calib_copy_mib:
