@@ -21,10 +21,11 @@ same inputs and permutation, timed, and (with the CPU leg) both compared with ex
 exponentiate-then-cast) on the main layer and its permutation, attention timed per mode and (with
 the CPU leg) compared with exact fp64 attention.
 
-`--grouping-study` runs only the token-order study instead (see `grouping_study`).
+`--grouping-study` runs only the token-order study instead (see `grouping_study`), `--prep-ladder`
+only the preprocessing fusion ladder (see `prep_ladder`).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra] [--mx4-only]
-                       [--grouping-study]
+                       [--grouping-study] [--prep-ladder]
 """
 from __future__ import annotations
 
@@ -432,6 +433,112 @@ def grouping_study(vc, S, n_host_heads=8, reps=5):
             "attn_ms": t_attn, "host_heads": len(host_heads), "rows": rows}
 
 
+def prep_ladder(vc, S, reps=10):
+    """The preprocessing chain on the main layer, fused into the quantizers one stage at a time
+    (cumulative rungs; eager stages are PyTorch operations that each write their full result to
+    HBM, bf16 between stages as an eager model would keep activations):
+      R0 every stage eager (fp32 intermediates; the quantizers too);
+      R1 quantizers + Hadamard fused (library prep with RoPE, centering and demeaning off, on
+         eagerly rotated, centred, gathered and demeaned bf16 inputs; block means eager);
+      R2 + the smoothing means and the gather fused (only the rotary embedding eager);
+      R3 + the rotary embedding fused (the library's prep as the method runs it).
+    Each rung is timed over `reps` calls with HIP events; the permutation comes from one k-means
+    grouping. Codes of R1 and R2 are compared byte for byte with R3's."""
+    import torch
+    w = S.WORKLOADS[WORKLOAD]
+    B, H, N, grid = w.B, w.H, w.N, w.grid
+    F_, Ht, Wd = grid
+    T = (N + 127) // 128
+    Np = 128 * T
+    print("[bench] prep ladder: inputs", file=sys.stderr, flush=True)
+    Qh, Kh, Vh = S.make_qkv(WORKLOAD, seed=0)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    Q, K, V = dev(Qh), dev(Kh), dev(Vh)
+    A3 = vc.Attention(B, H, grid)
+    A3.group(V)
+    perm = A3.perm.clone()
+    perm64 = perm.long()
+    # per-token rotary tables [N, 64] from the library's per-axis tables
+    cos_t, sin_t = (torch.from_numpy(t).cuda() for t in vc.rope_tables_host(F_, Ht, Wd))
+    n = torch.arange(N, device="cuda")
+    f, y, x = n // (Ht * Wd), (n // Wd) % Ht, n % Wd
+    pidx = torch.arange(64, device="cuda")
+    row = torch.where(pidx[None, :] < 22, f[:, None], torch.where(pidx[None, :] < 43, F_ + y[:, None], F_ + Ht + x[:, None]))
+    cos_n, sin_n = cos_t[row, pidx[None, :]], sin_t[row, pidx[None, :]]
+    Hm = torch.from_numpy(__import__("scipy.linalg", fromlist=["hadamard"]).hadamard(128).astype(np.float32)).cuda()
+    bf = lambda t: t.view(torch.bfloat16)
+    as_bits = lambda t: t.to(torch.bfloat16).view(torch.int16)
+    cnt = torch.clamp(N - 128 * torch.arange(T, device="cuda"), max=128).float()
+
+    def rope(xb):
+        xx = bf(xb).float().view(B, H, N, 64, 2)
+        y0 = xx[..., 0] * cos_n - xx[..., 1] * sin_n
+        y1 = xx[..., 0] * sin_n + xx[..., 1] * cos_n
+        return torch.stack((y0, y1), -1).view(B, H, N, 128)
+
+    def gather(t):
+        return torch.gather(t, 2, perm64[..., None].expand(-1, -1, -1, 128))
+
+    def block_means(vg):
+        vp = torch.nn.functional.pad(vg, (0, 0, 0, Np - N)).view(B, H, T, 128, 128)
+        return (vp.sum(3) / cnt[None, None, :, None]).to(torch.bfloat16).float()
+
+    def demean(vg, mu):
+        return vg - mu.repeat_interleave(128, dim=2)[:, :, :N]
+
+    def rung0():
+        qr, kr = rope(Q), rope(K)
+        kc = kr - kr.mean(dim=2, keepdim=True)
+        kg, vg = gather(kc), gather(bf(V).float())
+        mu = block_means(vg)
+        res = demean(vg, mu)
+        outs = []
+        for t in (qr, kg):
+            th = torch.nn.functional.pad(t, (0, 0, 0, Np - N)) @ Hm
+            sc = th.view(B, H, T, -1).abs().amax(-1).clamp_min(1e-30) / 127.0
+            outs.append(torch.round(th / sc.repeat_interleave(128, dim=2)[..., None]).clamp(-127, 127).to(torch.int8))
+        vs = res.abs().amax(dim=2, keepdim=True) / 448.0
+        outs.append((res / vs).to(torch.float8_e4m3fn))
+        return outs
+
+    A1 = vc.Attention(B, H, grid, vc.make_opts(rope=False, smooth_k=False, smooth_v=False),
+                      vc.make_group_opts(mode=vc.GROUP_IDENTITY))
+    A2 = vc.Attention(B, H, grid, vc.make_opts(rope=False))
+    A2.perm.copy_(perm)
+
+    def rung1():
+        qr, kr = as_bits(rope(Q)), rope(K)
+        kc = as_bits(gather(kr - kr.mean(dim=2, keepdim=True)))
+        vg = gather(bf(V).float())
+        mu = block_means(vg)
+        res = as_bits(demean(vg, mu))
+        A1.prep(qr, kc, res, perm=None)
+        return mu
+
+    def rung2():
+        A2.prep(as_bits(rope(Q)), as_bits(rope(K)), V)
+
+    def rung3():
+        A3.prep(Q, K, V)
+
+    ms = []
+    for fn in (rung0, rung1, rung2, rung3):
+        time_stages([fn], 2)
+        ms.append(time_stages([fn], reps)[0])
+    same = lambda a, b: float((a.view(torch.uint8) == b.view(torch.uint8)).float().mean().item())
+    p1, p2, p3 = A1.prepped, A2.prepped, A3.prepped
+    agree = {"R1": {k: same(getattr(p1, k), getattr(p3, k)) for k in ("q", "k", "v")},
+             "R2": {k: same(getattr(p2, k), getattr(p3, k)) for k in ("q", "k", "v")}}
+    names = ["R0 all stages eager", "R1 quantizers + Hadamard fused", "R2 + means and gather fused",
+             "R3 + rotary embedding fused (library prep)"]
+    alg = prep_algorithmic_bytes(B, H, N)
+    return {"workload": f"B={B} H={H} N={N} (grid {F_}x{Ht}x{Wd}) d=128, k-means permutation",
+            "algorithmic_bytes_fused": alg,
+            "rungs": [{"rung": nm, "ms": t, "speedup_vs_R0": ms[0] / t, "gbs_of_fused_bytes": alg / (t * 1e-3) / 1e9}
+                      for nm, t in zip(names, ms)],
+            "code_agreement_with_R3": agree}
+
+
 def mx4_accuracy(sample):
     """rel-L2 and PSNR of both formats' GPU outputs against exact fp64 attention (oracle) on the
     sampled rows."""
@@ -453,6 +560,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the denoising-loop slice and the large layer (reported beside the main line)")
+    ap.add_argument("--prep-ladder", action="store_true",
+                    help="run only the preprocessing fusion ladder (eager chain to fused kernels) and print it")
     ap.add_argument("--grouping-study", action="store_true",
                     help="run only the token-order study (energy removed, value error, overhead) and print it")
     ap.add_argument("--mx4-only", action="store_true",
@@ -473,6 +582,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.prep_ladder:
+        print(json.dumps({"prep_ladder": prep_ladder(vc, S)}), flush=True)
+        return
     if args.grouping_study:
         print(json.dumps({"grouping_study": grouping_study(vc, S)}), flush=True)
         return
