@@ -60,7 +60,7 @@ size_t group_ws(const vc_shape* s, const vc_group_opts* g) {
   if (g->mode != VC_GROUP_KMEANS) return 0;
   const size_t BH = (size_t)s->B * s->H, N = s->N, K = g->k, nblk = blocks_of(s->N, 256);
   return align256(BH * N * kD) + align256(BH * 4) + align256(BH * K * kD * 4) + align256(BH * nblk * K * kD * 4) +
-         2 * align256(BH * nblk * K * 4) + align256(BH * blocks_of(s->N, 32) * 32 * kD) + align256(BH * 64 * kD) +
+         2 * align256(BH * nblk * K * 4) + align256(BH * 64 * kD) +
          align256(BH * 64 * 4);
 }
 
@@ -184,8 +184,6 @@ vc_status vc_attn_group(const vc_shape* shape, const vc_group_opts* gopts, const
     p += align256(BH * nblk * K * 4);
     a.blockhist = reinterpret_cast<int32_t*>(p);
     p += align256(BH * nblk * K * 4);
-    a.codesT = reinterpret_cast<int8_t*>(p);
-    p += align256(BH * blocks_of(N, 32) * 32 * kD);
     a.cent8 = reinterpret_cast<int8_t*>(p);
     p += align256(BH * 64 * kD);
     a.cnorm = reinterpret_cast<int32_t*>(p);

@@ -2,17 +2,16 @@
 // are clustered and the keys/values are later gathered in cluster order.
 //
 // KMEANS: Lloyd rounds on per-head INT8 codes of V (scale amax/127 over the head).
-//   grp_amax     per-head max |V| (exact, order-free: integer max of non-negative float bits)
-//   grp_codes    INT8 codes, row-major [N][128], plus a token-interleaved copy for the member
-//                sums (per 32-token block, per 32-channel block and lane half: 16 consecutive
-//                tokens of one channel; transposed through LDS)
+//   grp_amax     per-head max |V|, one partial maximum per 256 tokens (max is order-free)
+//   grp_codes    the head's maximum from the partials, INT8 codes, row-major [N][128]
 //   grp_init     initial integer centroids (tokens floor((2c+1)N/(2k)), or the caller's fp32
 //                centroids requantized)
-//   grp_assign   1024 tokens per workgroup, 32 per wave step, on the matrix cores: the INT8
+//   grp_assign   1024 tokens per workgroup in chunks of 256, on the matrix cores: the INT8
 //                product C X^T gives |C|^2 - 2 x.C exactly in int32, the argmin is one integer
 //                min over (distance << 7 | cluster) (ties to the smallest cluster); then the
-//                exact member sums O X with the one-hot label matrix O as the INT8 A operand,
-//                and the counts (partials per workgroup, reduced by grp_update)
+//                exact member sums O X with the one-hot label matrix O as the INT8 A operand
+//                (the chunk's codes transposed through LDS), and the counts (partials per
+//                workgroup, reduced by grp_update)
 //   grp_update   centroid = round-half-even integer mean of the members (exact int64 division)
 // Integer arithmetic throughout makes labels, centroids and the permutation reproducible bit for
 // bit regardless of the order in which partial sums are combined.
@@ -28,100 +27,67 @@ namespace vc {
 constexpr int GT = 256;   // tokens per assignment / sort block
 constexpr int KMAX = 64;  // clusters supported by the kernels
 
-__global__ void grp_zero(uint32_t* p, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0u;
-}
-
-// Each workgroup reduces 64 KB of the head (16 chunks of 16 bytes per thread) before one atomic.
+// Each workgroup reduces 64 KB of the head (16 chunks of 16 bytes per thread, all loads issued
+// before the first use; chunks past the head's end re-read its last chunk) to one partial maximum.
 __global__ __launch_bounds__(256) void grp_amax(GroupArgs a) {
   __shared__ float red[4];
   const int bh = blockIdx.y;
   const size_t words = (size_t)a.N * D / 8;  // 16-byte chunks of the head
   const u4* src = reinterpret_cast<const u4*>(a.V + (size_t)bh * a.N * D);
+  u4 w[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) w[u] = src[min(((size_t)blockIdx.x * 16 + u) * 256 + threadIdx.x, words - 1)];
   float m = 0.f;
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const size_t i = ((size_t)blockIdx.x * 16 + u) * 256 + threadIdx.x;
-    if (i < words) {
-      const u4 w = src[i];
+  for (int u = 0; u < 16; ++u)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[q])), fabsf(bf16_hi(w[q]))));
-    }
-  }
+    for (int q = 0; q < 4; ++q) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[u][q])), fabsf(bf16_hi(w[u][q]))));
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
   __syncthreads();
-  if (threadIdx.x == 0)
-    atomicMax(reinterpret_cast<unsigned int*>(a.scale) + bh,
-              __float_as_uint(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
+  if (threadIdx.x == 0)   // one partial per workgroup (gridDim.x = nblk), reduced by grp_codes
+    reinterpret_cast<float*>(a.counts)[(size_t)bh * gridDim.x + blockIdx.x] =
+        fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
 __device__ __forceinline__ float head_amax(const GroupArgs& a, int bh) { return a.scale[bh]; }
 
-// 256 tokens per workgroup: each thread quantizes one token into its row-major row and into LDS;
-// then 4x4 byte transposes through LDS write the token-interleaved copy with 16-byte stores.
+// 256 tokens per workgroup: consecutive threads quantize consecutive 16-byte chunks of the
+// workgroup's rows (8 channels each) and store the 8 code bytes, so loads and stores coalesce.
 __global__ __launch_bounds__(256) void grp_codes(GroupArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t xs[256][D / 4 + 1];
+  __shared__ float red[4];
   const int bh = blockIdx.y, t = threadIdx.x;
-  const int n = blockIdx.x * 256 + t;
-  const float amax = head_amax(a, bh);
-  const float inv = amax > 0.f ? 127.f / amax : 0.f;
-  if (n < a.N) {
-    const u4* src = reinterpret_cast<const u4*>(a.V + ((size_t)bh * a.N + n) * D);
-    u4* dst = reinterpret_cast<u4*>(a.codes + ((size_t)bh * a.N + n) * D);
+  const int n0 = blockIdx.x * 256;
+  const int ntok = min(256, a.N - n0);
+  // the head's |V| maximum from grp_amax's partials (one per 256-token block; max is order-free)
+  float pm = 0.f;
+  for (int i = t; i < (int)gridDim.x; i += 256) pm = fmaxf(pm, reinterpret_cast<const float*>(a.counts)[(size_t)bh * gridDim.x + i]);
 #pragma unroll
-    for (int ch = 0; ch < 8; ++ch) {   // 16 channels per chunk
-      const u4 w0 = src[2 * ch], w1 = src[2 * ch + 1];
-      uint32_t out[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t w = q < 2 ? w0[2 * q] : w1[2 * (q - 2)];
-        const uint32_t v = q < 2 ? w0[2 * q + 1] : w1[2 * (q - 2) + 1];
-        float f[4] = {bf16_lo(w), bf16_hi(w), bf16_lo(v), bf16_hi(v)};
-        uint32_t pk = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float r = __builtin_rintf(f[e] * inv);
-          r = fminf(fmaxf(r, -127.f), 127.f);
-          pk |= ((uint32_t)((int)r & 0xff)) << (8 * e);
-        }
-        out[q] = pk;
-        xs[t][4 * ch + q] = pk;
-      }
-      dst[ch] = u4{out[0], out[1], out[2], out[3]};
-    }
-  } else {
-#pragma unroll
-    for (int w = 0; w < D / 4; ++w) xs[t][w] = 0u;   // padded tokens: zero codes
-  }
+  for (int o = 32; o >= 1; o >>= 1) pm = fmaxf(pm, __shfl_xor(pm, o));
+  if ((t & 63) == 0) red[t >> 6] = pm;
   __syncthreads();
-  // unit (block b of 32 tokens, lane half kh, channels 4g..4g+3): 16 tokens x 4 channels
-  const int ntb = (a.N + 31) / 32;
+  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  if (blockIdx.x == 0 && t == 0) a.scale[bh] = amax;   // for the centroid kernels
+  const float inv = amax > 0.f ? 127.f / amax : 0.f;
+  const u4* src = reinterpret_cast<const u4*>(a.V + ((size_t)bh * a.N + n0) * D);
+  uint2* dst = reinterpret_cast<uint2*>(a.codes + ((size_t)bh * a.N + n0) * D);
+  u4 w[16];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int unit = u * 256 + t;
-    const int g = unit & 31, kh = (unit >> 5) & 1, b = unit >> 6;
-    const int tb = blockIdx.x * 8 + b;
-    if (tb >= ntb) continue;
-    uint32_t col[4][4];   // col[j][tq]: channel 4g+j of tokens 4tq..4tq+3 (of the 16)
+  for (int u = 0; u < 16; ++u) w[u] = src[min(u * 256 + t, ntok * 16 - 1)];   // chunks of padded tokens re-read the last one
 #pragma unroll
-    for (int tq = 0; tq < 4; ++tq) {
-      uint32_t r[4];
+  for (int u = 0; u < 16; ++u) {
+    const int q = u * 256 + t;
+    if ((q >> 4) >= ntok) continue;
+    uint32_t pk[2] = {0u, 0u};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) r[e] = xs[b * 32 + kh * 16 + 4 * tq + e][g];
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        col[j][tq] = ((r[0] >> (8 * j)) & 0xffu) | (((r[1] >> (8 * j)) & 0xffu) << 8) |
-                     (((r[2] >> (8 * j)) & 0xffu) << 16) | (((r[3] >> (8 * j)) & 0xffu) << 24);
+    for (int e = 0; e < 8; ++e) {
+      const float f = (e & 1) ? bf16_hi(w[u][e >> 1]) : bf16_lo(w[u][e >> 1]);
+      float r = __builtin_rintf(f * inv);
+      r = fminf(fmaxf(r, -127.f), 127.f);
+      pk[e >> 2] |= ((uint32_t)((int)r & 0xff)) << (8 * (e & 3));
     }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = 4 * g + j, db = c >> 5, cl = c & 31;
-      u4* dst = reinterpret_cast<u4*>(a.codesT + ((size_t)bh * ntb + tb) * (32 * D) + (((db * 2 + kh) * 32 + cl) * 16));
-      *dst = u4{col[j][0], col[j][1], col[j][2], col[j][3]};
-    }
+    dst[q] = make_uint2(pk[0], pk[1]);
   }
 }
 
@@ -163,26 +129,31 @@ __global__ __launch_bounds__(D) void grp_init(GroupArgs a) {
   publish_centroid(a, bh, k, c, v);
 }
 
-constexpr int AW = 4;            // waves per assignment workgroup
-constexpr int AG = 8;            // 32-token steps per wave
-constexpr int ATOK = AW * AG * 32;   // 1024 tokens per assignment workgroup
+constexpr int AW = 8;            // waves per assignment workgroup
+constexpr int ATOK = 1024;       // tokens per assignment workgroup (one partial each)
+constexpr int ACH = 256;         // tokens per chunk: one 32-token label step per wave
+constexpr int NCH = ATOK / ACH;
 
-// One Lloyd assignment on the matrix cores (KB = clusters / 32, rounded up). Per 32-token step:
+// One Lloyd assignment on the matrix cores (KB = clusters / 32, rounded up), chunk by chunk.
+// Labels (wave w: tokens 32w .. 32w + 31 of the chunk):
 //   S^T = C X^T     INT8 MFMA 32x32x32, A = centroid rows (registers), B = the tokens' codes;
 //                   lane (token l%32, half l/32) holds 16 clusters' x.C, the other 16 in lane l^32
 //   key  = (|C|^2 - 2 x.C + 2^23) << 7 | cluster, argmin = integer min of the keys (the distance
 //          fits 24 bits, the cluster 7 bits; equal distances resolve to the smaller cluster)
-//   sums += O X     INT8 MFMA, A = one-hot labels (cluster rows x 32 tokens), B = the
-//                   token-interleaved codes (16 consecutive tokens of one channel per lane)
-//   counts         popcounts of the one-hot bytes
-// The wave's sums stay in registers; at the end they are added into LDS and written as one
-// partial per workgroup.
+//   the label goes to memory, to the chunk's label row in LDS and to its cluster's count; the
+//   codes go to the chunk's LDS rows.
+// Sums (wave w: byte w%4 of every 4-channel word, i.e. channels 4c + w%4, half w/4 of the chunk):
+//   sums += O X     INT8 MFMA, A = one-hot labels (cluster rows x 32 tokens), B = 16 consecutive
+//                   tokens of channel 4 col + w%4 per lane, gathered from the LDS rows
+// Each wave keeps 16 sum registers per cluster block. The sums are added into LDS and written as
+// one partial per workgroup; all arithmetic is integer, so the order of additions is free.
 template <int KB>
 __global__ __launch_bounds__(AW * 64) void grp_assign(GroupArgs a) {
   __shared__ int32_t acc[KB * 32][D];
   __shared__ int32_t cntl[KB * 32];
   __shared__ int32_t norm[KB * 32];
-  __shared__ __attribute__((aligned(16))) uint8_t lab[AW][32];
+  __shared__ __attribute__((aligned(16))) uint8_t lab[ACH];
+  __shared__ __attribute__((aligned(16))) uint32_t xs[ACH][D / 4 + 2];   // 136-byte rows: no bank conflicts
   const int bh = blockIdx.y, wg = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kh = lane >> 5, col = lane & 31, K = a.k, N = a.N;
@@ -191,6 +162,8 @@ __global__ __launch_bounds__(AW * 64) void grp_assign(GroupArgs a) {
     norm[tid] = a.cnorm[(size_t)bh * KMAX + tid];
     cntl[tid] = 0;
   }
+  const int8_t* codes = a.codes + (size_t)bh * N * D;
+  const int wbase = wg * ATOK;
   // centroid rows as the A operand (padding clusters are zero rows) and the lane's norms
   v4i ca[KB][4];
   int32_t nr[KB][16];
@@ -199,102 +172,116 @@ __global__ __launch_bounds__(AW * 64) void grp_assign(GroupArgs a) {
 #pragma unroll
     for (int dc = 0; dc < 4; ++dc)
       ca[cb][dc] = *reinterpret_cast<const v4i*>(a.cent8 + ((size_t)bh * KMAX + 32 * cb + col) * D + 32 * dc + 16 * kh);
+  // the lane's codes (token 32 wave + col of a chunk, channels 32 dc + 16 kh ..), one chunk ahead
+  auto load_codes = [&](int c, v4i (&x)[4]) __attribute__((always_inline)) {
+    const int8_t* xr = codes + (size_t)min(wbase + c * ACH + 32 * wave + col, N - 1) * D + 16 * kh;
+#pragma unroll
+    for (int dc = 0; dc < 4; ++dc) x[dc] = *reinterpret_cast<const v4i*>(xr + 32 * dc);
+  };
+  v4i xb[4];
+  load_codes(0, xb);
   __syncthreads();
 #pragma unroll
   for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) nr[cb][r] = norm[32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3)];
-
-  const int ntb = (N + 31) / 32;
-  const int8_t* codes = a.codes + (size_t)bh * N * D;
-  const int8_t* codesT = a.codesT + (size_t)bh * ntb * (32 * D);
-  v16i sums[KB][4];
+  const int db = wave & 3, half = wave >> 2;
+  // byte db of each of two words -> bytes 0, 1 (lo) or 2, 3 (hi) of the result
+  const uint32_t sel_lo = 0x0c0c0000u | ((uint32_t)(4 + db) << 8) | (uint32_t)db;
+  const uint32_t sel_hi = ((uint32_t)(4 + db) << 24) | ((uint32_t)db << 16) | 0x0c0cu;
+  v16i sums[KB];
 #pragma unroll
   for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sums[cb][db][r] = 0;
-  int32_t cntp[KB];
-#pragma unroll
-  for (int cb = 0; cb < KB; ++cb) cntp[cb] = 0;
+    for (int r = 0; r < 16; ++r) sums[cb][r] = 0;
 
-  auto load_step = [&](int n0, v4i (&xb)[4], v4i (&xt)[4]) {
-    const int token = min(n0 + col, N - 1);
-    const int8_t* xr = codes + (size_t)token * D + 16 * kh;
+  for (int c = 0; c < NCH; ++c) {
+    const int cbase = wbase + c * ACH;
+    if (cbase >= N) break;   // uniform over the workgroup
+    {
+      const int n0 = cbase + 32 * wave;
+      int best = 0x7fffffff;
 #pragma unroll
-    for (int dc = 0; dc < 4; ++dc) xb[dc] = *reinterpret_cast<const v4i*>(xr + 32 * dc);
-    const int8_t* xc = codesT + (size_t)(n0 >> 5) * (32 * D) + (kh * 32 + col) * 16;
+      for (int cb = 0; cb < KB; ++cb) {
+        v16i S = {};
 #pragma unroll
-    for (int db = 0; db < 4; ++db) xt[db] = *reinterpret_cast<const v4i*>(xc + db * 1024);
-  };
-  const int nbase = wg * ATOK + wave * (AG * 32);
-  v4i xb[4], xt[4];
-  if (nbase < N) load_step(nbase, xb, xt);
-  for (int g = 0; g < AG; ++g) {
-    const int n0 = nbase + g * 32;
-    if (n0 >= N) break;
-    v4i xbn[4], xtn[4];
-    if (g + 1 < AG && n0 + 32 < N) load_step(n0 + 32, xbn, xtn);   // next step's codes in flight
-    int best = 0x7fffffff;
+        for (int dc = 0; dc < 4; ++dc) S = __builtin_amdgcn_mfma_i32_32x32x32_i8(ca[cb][dc], xb[dc], S, 0, 0, 0);
 #pragma unroll
-    for (int cb = 0; cb < KB; ++cb) {
-      v16i S = {};
-#pragma unroll
-      for (int dc = 0; dc < 4; ++dc) S = __builtin_amdgcn_mfma_i32_32x32x32_i8(ca[cb][dc], xb[dc], S, 0, 0, 0);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = ((nr[cb][r] - 2 * S[r] + (1 << 23)) << 7) | (32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3));
-        best = min(best, key);
+        for (int r = 0; r < 16; ++r) {
+          const int key = ((nr[cb][r] - 2 * S[r] + (1 << 23)) << 7) | (32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3));
+          best = min(best, key);
+        }
       }
-    }
-    best = min(best, __shfl_xor(best, 32));
-    const int token = n0 + col;
-    const bool valid = token < N;
-    const int label = valid ? (best & 127) : 255;
-    if (valid && kh == 0) a.labels[(size_t)bh * N + token] = label;
-    if (kh == 0) lab[wave][col] = (uint8_t)label;
-    // the wave's 32 labels: one-hot bytes of (cluster row, token) for this lane's 16 tokens
-    const u4 l4 = *reinterpret_cast<const u4*>(&lab[wave][16 * kh]);
+      best = min(best, __shfl_xor(best, 32));
+      const int token = n0 + col;
+      const bool valid = token < N;
+      const int label = valid ? (best & 127) : 255;
+      if (kh == 0) {
+        lab[32 * wave + col] = (uint8_t)label;
+        if (valid) {
+          a.labels[(size_t)bh * N + token] = label;
+          atomicAdd(&cntl[label], 1);
+        }
+      }
+      // codes into the chunk's LDS rows (tokens past N: zero codes); rows are 136 bytes, so the
+      // stores are 8-byte ones
 #pragma unroll
-    for (int cb = 0; cb < KB; ++cb) {
-      const uint32_t rep = (uint32_t)(32 * cb + col) * 0x01010101u;
-      int32_t oh[4];
+      for (int dc = 0; dc < 4; ++dc) {
+        const v4i v = valid ? xb[dc] : v4i{0, 0, 0, 0};
+        uint2* d = reinterpret_cast<uint2*>(&xs[32 * wave + col][8 * dc + 4 * kh]);
+        d[0] = make_uint2((uint32_t)v[0], (uint32_t)v[1]);
+        d[1] = make_uint2((uint32_t)v[2], (uint32_t)v[3]);
+      }
+      if (c + 1 < NCH) load_codes(c + 1, xb);   // the next chunk's codes in flight
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      const int t0 = 128 * half + 32 * s4;   // step's first token in the chunk
+      if (cbase + t0 >= N) break;
+      // operand: tokens t0 + 16 kh .. + 15 of channel 4 col + db, byte i = token i
+      int32_t xv[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t x = l4[q] ^ rep;
-        const uint32_t nz = (((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x) & 0x80808080u;   // 0x80 where byte != 0
-        oh[q] = (int32_t)((~nz >> 7) & 0x01010101u);
-        cntp[cb] += __builtin_popcount((uint32_t)oh[q]);
+        const int r0 = t0 + 16 * kh + 4 * q;
+        const uint32_t lo = __builtin_amdgcn_perm(xs[r0 + 1][col], xs[r0][col], sel_lo);
+        const uint32_t hi = __builtin_amdgcn_perm(xs[r0 + 3][col], xs[r0 + 2][col], sel_hi);
+        xv[q] = (int32_t)(lo | hi);
       }
-      const v4i ohv = {oh[0], oh[1], oh[2], oh[3]};
+      const v4i xop = {xv[0], xv[1], xv[2], xv[3]};
+      const u4 l4 = *reinterpret_cast<const u4*>(&lab[t0 + 16 * kh]);
 #pragma unroll
-      for (int db = 0; db < 4; ++db) sums[cb][db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ohv, xt[db], sums[cb][db], 0, 0, 0);
-    }
-    if (g + 1 < AG && n0 + 32 < N) {
+      for (int cb = 0; cb < KB; ++cb) {
+        const uint32_t rep = (uint32_t)(32 * cb + col) * 0x01010101u;
+        int32_t oh[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { xb[q] = xbn[q]; xt[q] = xtn[q]; }
-    }
-  }
-  // this wave's sums and counts into the workgroup's LDS accumulators
-#pragma unroll
-  for (int cb = 0; cb < KB; ++cb) {
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3);
-        if (row < K) atomicAdd(&acc[row][32 * db + col], sums[cb][db][r]);
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t x = l4[q] ^ rep;
+          const uint32_t nz = (((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x) & 0x80808080u;   // 0x80 where byte != 0
+          oh[q] = (int32_t)((~nz >> 7) & 0x01010101u);
+        }
+        const v4i ohv = {oh[0], oh[1], oh[2], oh[3]};
+        sums[cb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ohv, xop, sums[cb], 0, 0, 0);
       }
-    if (32 * cb + col < K) atomicAdd(&cntl[32 * cb + col], cntp[cb]);
+    }
+    __syncthreads();   // the next chunk overwrites the rows and labels
   }
+  // this wave's sums (rows = clusters, column col = channel 4 col + db) into the LDS accumulators
+#pragma unroll
+  for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 32 * cb + 8 * (r >> 2) + 4 * kh + (r & 3);
+      if (row < K) atomicAdd(&acc[row][4 * col + db], sums[cb][r]);
+    }
   __syncthreads();
   const size_t part = (size_t)bh * a.npart + wg;
   for (int i = tid; i < K * D; i += AW * 64) a.sums[part * K * D + i] = (&acc[0][0])[i];
   if (tid < K) a.counts[part * K + tid] = cntl[tid];
 }
 
-// per-256-token-block label counts of the final labels (the stable sort's histogram)
+// per-256-token-block label counts of the final labels (the stable sort's histogram), stored
+// label-major [lab][blk]
 __global__ __launch_bounds__(GT) void grp_hist(GroupArgs a) {
   __shared__ int32_t h[KMAX];
   const int blk = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
@@ -303,7 +290,7 @@ __global__ __launch_bounds__(GT) void grp_hist(GroupArgs a) {
   const int n = blk * GT + t;
   if (n < a.N) atomicAdd(&h[a.labels[(size_t)bh * a.N + n]], 1);
   __syncthreads();
-  if (t < a.nlab) a.counts[((size_t)bh * a.nblk + blk) * a.nlab + t] = h[t];
+  if (t < a.nlab) a.counts[((size_t)bh * a.nlab + t) * a.nblk + blk] = h[t];
 }
 
 __device__ __forceinline__ int32_t div_rne(long long num, long long den) {
@@ -339,28 +326,31 @@ __global__ __launch_bounds__(128) void grp_cent_out(GroupArgs a) {
   a.centroids[i] = (float)a.cent[i] * scale;
 }
 
-// label-major exclusive offsets of the per-block label counts: off[k][b]
+// label-major exclusive offsets of the per-block label counts: off[k][b]. Each thread sums a
+// contiguous run of the label-major counts, a scan over the 256 run sums, then each thread writes
+// its run's offsets.
 __global__ __launch_bounds__(256) void grp_offsets(GroupArgs a) {
   __shared__ int32_t part[256];
   const int bh = blockIdx.x, t = threadIdx.x;
   const int total = a.nlab * a.nblk;
   const int per = (total + 255) / 256;
   const int lo = min(total, t * per), hi = min(total, lo + per);
-  const int32_t* cnt = a.counts + (size_t)bh * a.nblk * a.nlab;   // [blk][lab]
+  const int32_t* cnt = a.counts + (size_t)bh * a.nblk * a.nlab;   // [lab][blk]
   int32_t s = 0;
-  for (int idx = lo; idx < hi; ++idx) s += cnt[(size_t)(idx % a.nblk) * a.nlab + idx / a.nblk];
+  for (int idx = lo; idx < hi; ++idx) s += cnt[idx];
   part[t] = s;
   __syncthreads();
-  if (t == 0) {
-    int32_t run = 0;
-    for (int i = 0; i < 256; ++i) { const int32_t v = part[i]; part[i] = run; run += v; }
+  for (int o = 1; o < 256; o <<= 1) {   // inclusive scan (integers: exact in any order)
+    const int32_t v = t >= o ? part[t - o] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
   }
-  __syncthreads();
-  int32_t run = part[t];
+  int32_t run = part[t] - s;
   int32_t* off = a.blockhist + (size_t)bh * a.nlab * a.nblk;   // [lab][blk]
   for (int idx = lo; idx < hi; ++idx) {
     off[idx] = run;
-    run += cnt[(size_t)(idx % a.nblk) * a.nlab + idx / a.nblk];
+    run += cnt[idx];
   }
 }
 
@@ -417,9 +407,8 @@ hipError_t launch_group(const GroupArgs& a, int BH, hipStream_t s) {
     grp_cube<<<tok, 256, 0, s>>>(a);
     return hipGetLastError();
   }
-  grp_zero<<<(BH + 255) / 256, 256, 0, s>>>(reinterpret_cast<uint32_t*>(a.scale), BH);
-  const size_t words = (size_t)a.N * D / 8;
-  grp_amax<<<dim3((unsigned)((words + 4095) / 4096), BH), 256, 0, s>>>(a);
+  // grp_amax's grid (16 chunks of 16 bytes per thread = 256 tokens per workgroup) equals grp_codes'
+  grp_amax<<<tok, 256, 0, s>>>(a);
   grp_codes<<<tok, 256, 0, s>>>(a);
   grp_init<<<dim3(KMAX, BH), D, 0, s>>>(a);
   const int rounds = a.iters > 0 ? a.iters : 1;

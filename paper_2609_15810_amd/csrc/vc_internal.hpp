@@ -52,7 +52,6 @@ struct GroupArgs {
   float* centroids;
   int32_t *labels, *perm, *inv_perm;
   int8_t* codes;     // workspace: per-head INT8 codes of V [B*H][N][128]
-  int8_t* codesT;    // workspace: the same codes token-interleaved [B*H][ceil(N/32)][4][2][32][16]
   float* scale;      // workspace: [B*H] amax (then scale)
   int32_t* cent;     // workspace: [B*H][k][128] integer centroids
   int8_t* cent8;     // workspace: [B*H][64][128] the same as int8, rows k.. zero
