@@ -212,3 +212,34 @@ def test_mx4_h40_full_vs_8bit():
     # loose sanity bound: on this shape the 4-bit scores leave about 14% rel-L2 (PSNR ~43 dB) against
     # ~1.1% (~65 dB) for the 8-bit path
     assert rel["mxfp4"] < 0.25 and rel["int8"] < rel["mxfp4"], rel
+
+
+@pytest.mark.timeout(900)
+def test_modes_full_size():
+    """The 32760-token layer in the other modes, on the oracle's k-means permutation: the
+    exponentiate-then-cast probability path with INT8 scores, and FP8 scores with ExpCast (the
+    FP8 product's accumulation error enters through the derived per-row bound); sampled rows of
+    three heads."""
+    from test_gpu_fp8qk import check_output_f8, flip_bound
+    name = "dit_small"
+    w = S.WORKLOADS[name]
+    log("generating inputs")
+    Q, K, V = S.make_qkv(name, seed=0)
+    g = oracle.group(V, w.grid, k=32, iters=8)
+    perm = torch.from_numpy(np.ascontiguousarray(g["perm"])).cuda()
+    rows = sample_rows(w.N)
+    heads = [0, 5, 11]
+    for qk, pm, tag in ((vc.QK_INT8, vc.P_EXP_THEN_CAST, "int8 exp-then-cast"), (vc.QK_FP8, vc.P_EXPCAST, "fp8 expcast")):
+        log(f"GPU prep + forward, {tag}")
+        A = vc.Attention(w.B, w.H, w.grid, vc.make_opts(qk_fmt=qk, p_mode=pm))
+        A.perm.copy_(perm)
+        A, o = run_gpu(name, Q, K, V, A=A, regroup=False)
+        log(f"oracle on {rows.size} rows x {len(heads)} heads")
+        pph = oracle.prep(Q[:, heads], K[:, heads], V[:, heads], w.grid, perm=g["perm"][:, heads],
+                          qk_fmt=oracle.QK_FP8 if qk == vc.QK_FP8 else oracle.QK_INT8)
+        ref = oracle.attention(pph, rows, p_mode=pm)
+        if qk == vc.QK_FP8:
+            for t, h in enumerate(heads):
+                check_output_f8(o[h][rows], ref[t], flip_bound(pph, t, rows), f"{name} {tag} head {h}")
+        else:
+            check_output(o[heads][:, rows], ref, f"{name} {tag}")
