@@ -274,6 +274,40 @@ def attention(pp, rows, bh=None, p_mode=P_EXPCAST, sm_scale=None, beta=-0.35):
     return out
 
 
+def attention_codes(pp, rows, bh=None, p_mode=P_EXPCAST, sm_scale=None, beta=-0.35):
+    """The 8-bit probability codes of the recurrence for the given rows (prepared query order):
+    uint8 [len(bh), R, 128 T], key order of the prepared K' (padded keys 0), each tile's codes at
+    that tile's running maximum."""
+    B, H = pp["q"].shape[:2]
+    N = pp["N"]
+    T = (N + BLK - 1) // BLK
+    if sm_scale is None:
+        sm_scale = float(np.float32(1.0 / np.sqrt(D)))
+    rows = _c(rows, np.int32)
+    bh = list(range(B * H)) if bh is None else list(bh)
+    out = np.zeros((len(bh), rows.size, T * BLK), np.uint8)
+    qk_fmt = int(pp.get("qk_fmt", QK_INT8))
+    cfg = AttnCfg(N, int(pp["hadamard"]), int(pp["smooth_v"]), int(p_mode), float(sm_scale), float(beta), qk_fmt)
+    q = pp["q"].reshape(B * H, -1, D); qs = pp["q_scale"].reshape(B * H, -1)
+    k = pp["k"].reshape(B * H, -1, D); ks = pp["k_scale"].reshape(B * H, -1)
+    v = pp["v"].reshape(B * H, -1, D); vs = pp["v_scale"].reshape(B * H, D)
+    vm = pp["v_mean"].reshape(B * H, -1, D)
+    mx = qk_fmt == QK_MXFP4
+    if mx:
+        qm = pp["q_mx"].reshape(B * H, -1, D); qms = pp["q_mxs"].reshape(B * H, -1, 4)
+        km = pp["k_mx"].reshape(B * H, -1, D); kms = pp["k_mxs"].reshape(B * H, -1, 4)
+    scratch = np.zeros((rows.size, D), np.float64)
+    for t, h in enumerate(bh):
+        codes = np.zeros((rows.size, T * BLK), np.uint8)
+        mxargs = [_p(_c(a[h], np.uint8)) for a in (qm, qms, km, kms)] if mx else [None] * 4
+        lib().or_attn_head_codes(C.byref(cfg), _p(_c(q[h].view(np.int8), np.int8)), _p(_c(qs[h], np.float32)),
+                                 _p(_c(k[h].view(np.int8), np.int8)), _p(_c(ks[h], np.float32)),
+                                 _p(_c(v[h], np.uint8)), _p(_c(vs[h], np.float32)), _p(_c(vm[h], np.uint16)),
+                                 C.c_int(rows.size), _p(rows), _p(scratch), *mxargs, _p(codes))
+        out[t] = codes
+    return out
+
+
 def attention_tiled_f64(Qf, Kf, Vf, rows, sm_scale=None, smooth_v=True):
     """The online recurrence with block-mean restoration on full-precision rows of one head."""
     Qf, Kf, Vf = (_c(t, np.float64) for t in (Qf, Kf, Vf))

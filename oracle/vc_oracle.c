@@ -529,7 +529,7 @@ static float score_kappa(const or_attn_cfg *cfg)
 static void attn_row(const or_attn_cfg *cfg, int i, const int8_t *qc, const float *qs,
                      const int8_t *kc, const float *ks, const uint8_t *vc, const float *vs,
                      const uint16_t *vm, const uint8_t *qm, const uint8_t *qms, const uint8_t *km,
-                     const uint8_t *kms, double *out)
+                     const uint8_t *kms, double *out, uint8_t *codes_out)
 {
     const int N = cfg->N, T = (N + BLK - 1) / BLK;
     const int mx = cfg->qk_fmt == OR_QK_MXFP4;
@@ -578,6 +578,7 @@ static void attn_row(const or_attn_cfg *cfg, int i, const int8_t *qc, const floa
         for (int s = 0; s < valid; ++s) {
             int code = cfg->p_mode == OR_P_EXPCAST ? or_expcast_code_s(sc[s], a, m_new, cfg->beta)
                                                    : or_exp_then_cast_code_s(sc[s], a, m_new);
+            if (codes_out) codes_out[j * BLK + s] = (uint8_t)code;
             double p = or_e4m3_decode((uint8_t)code);
             if (p == 0.0) continue;
             r += p;
@@ -604,7 +605,24 @@ void or_attn_head(const or_attn_cfg *cfg, const int8_t *q_codes, const float *q_
 #pragma omp parallel for schedule(dynamic, 1)
     for (int t = 0; t < n_rows; ++t)
         attn_row(cfg, rows[t], q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, v_mean,
-                 q_mx, q_mxs, k_mx, k_mxs, &out[(size_t)t * D]);
+                 q_mx, q_mxs, k_mx, k_mxs, &out[(size_t)t * D], NULL);
+}
+
+/* The 8-bit probability codes the recurrence forms for the selected query rows: codes_out
+ * [n_rows x 128 T] (key order of the prepared K', padded keys 0), each tile's codes taken at that
+ * tile's running maximum. Same arguments as or_attn_head otherwise (out may be scratch). */
+void or_attn_head_codes(const or_attn_cfg *cfg, const int8_t *q_codes, const float *q_scale,
+                        const int8_t *k_codes, const float *k_scale, const uint8_t *v_codes,
+                        const float *v_scale, const uint16_t *v_mean, int n_rows, const int32_t *rows,
+                        double *out, const uint8_t *q_mx, const uint8_t *q_mxs, const uint8_t *k_mx,
+                        const uint8_t *k_mxs, uint8_t *codes_out)
+{
+    const int T = (cfg->N + BLK - 1) / BLK;
+    memset(codes_out, 0, (size_t)n_rows * T * BLK);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int t = 0; t < n_rows; ++t)
+        attn_row(cfg, rows[t], q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, v_mean,
+                 q_mx, q_mxs, k_mx, k_mxs, &out[(size_t)t * D], &codes_out[(size_t)t * T * BLK]);
 }
 
 /* The same online recurrence on full-precision operands (no quantizer, exact exponential):

@@ -143,3 +143,35 @@ def test_mean_restoration_is_exact_without_quantization():
     a = oracle.attention_tiled_f64(Qf, Kf, Vf, rows, smooth_v=True)
     b = oracle.attention_tiled_f64(Qf, Kf, Vf, rows, smooth_v=False)
     assert np.abs(a - b).max() < 1e-12
+
+
+def test_attention_codes_match_closed_form():
+    """The codes the oracle's recurrence exposes are the closed form's codes (tile-wise at the
+    tile's running maximum), padded keys 0."""
+    grid = (3, 5, 20)   # N = 300: tiles of 128, 128, 44 keys
+    rng = np.random.default_rng(19)
+    N = 300
+    Q = S.bf16_bits(rng.standard_normal((1, 1, N, 128)).astype(np.float32) * 2)
+    K = S.bf16_bits((rng.standard_normal((1, 1, N, 128)) * 2 + rng.standard_normal(128) * 3).astype(np.float32))
+    V = S.bf16_bits(rng.standard_normal((1, 1, N, 128)).astype(np.float32))
+    pp = oracle.prep(Q, K, V, grid, perm=S.random_perm(N, 2, 1, 1))
+    sm = float(np.float32(1 / np.sqrt(128)))
+    rows = np.array([0, 1, 127, 128, 200, 299], np.int32)
+    codes = oracle.attention_codes(pp, rows, sm_scale=sm)[0]
+    T = 3
+    q_all = pp["q"].reshape(-1, T * 128, 128)[0]
+    kc = pp["k"].reshape(-1, T * 128, 128)[0, :N].astype(np.int64)
+    qs, ks = pp["q_scale"][0, 0], pp["k_scale"][0, 0]
+    kappa = np.float32(sm * np.log2(np.e) / 128.0)
+    for t, i in enumerate(rows):
+        acc = kc @ q_all[i].astype(np.int64)
+        a = np.array([np.float32(np.float32(qs[i // 128] * ks[j]) * kappa) for j in range(T)], np.float32)
+        tmax = np.array([np.float32(np.float32(acc[128 * j:128 * (j + 1)].max()) * a[j]) for j in range(T)], np.float32)
+        m = np.maximum.accumulate(tmax)
+        want = np.zeros(T * 128, np.uint8)
+        for j in range(T):
+            sl = slice(128 * j, min(128 * (j + 1), N))
+            bias = np.float32(np.float32(np.float32(120.0) + np.float32(-0.35)) - np.float32(8.0) * m[j])
+            c = np.float32(acc[sl].astype(np.float64) * (8.0 * np.float64(a[j])) + np.float64(bias))
+            want[sl] = np.clip(np.rint(c), 0, 120).astype(np.uint8)
+        assert np.array_equal(codes[t], want), i
