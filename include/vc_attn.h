@@ -218,6 +218,18 @@ vc_status vc_attn_prep(const vc_shape *shape, const vc_opts *opts, const uint16_
 vc_status vc_attn_forward(const vc_shape *shape, const vc_opts *opts, const vc_prepped *in,
                           const int32_t *q_perm, uint16_t *O, void *stream);
 
+/* vc_attn_forward that also writes the 8-bit probability codes it forms (Sec. 3.3 eq.
+ * direct-fp8 in ExpCast mode, the FP8 cast of the exponentials otherwise), for debugging and
+ * parity checks; it waits for every tile copy in flight before each tile, so copies no longer
+ * overlap the computation.
+ *   p_codes : device uint8 [B, H, N, 128 T] (T = ceil(N / 128)), 16-byte aligned, caller-owned,
+ *             fully overwritten. Row i is the prepared query i (before q_perm); byte 128 t + s is
+ *             key s of tile t of the prepared K', coded at the running maximum after tile t;
+ *             keys past N are 0.
+ * Other arguments and errors as vc_attn_forward; VC_ERR_NULL if p_codes is NULL. */
+vc_status vc_attn_forward_codes(const vc_shape *shape, const vc_opts *opts, const vc_prepped *in,
+                                const int32_t *q_perm, uint16_t *O, uint8_t *p_codes, void *stream);
+
 /* Static description of a status code. */
 const char *vc_status_str(vc_status s);
 

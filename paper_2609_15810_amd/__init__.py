@@ -83,6 +83,9 @@ def lib():
         L.vc_attn_forward.restype = C.c_int
         L.vc_attn_forward.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.POINTER(Prepped), C.c_void_p,
                                       C.c_void_p, C.c_void_p]
+        L.vc_attn_forward_codes.restype = C.c_int
+        L.vc_attn_forward_codes.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.POINTER(Prepped), C.c_void_p,
+                                            C.c_void_p, C.c_void_p, C.c_void_p]
         L.vc_opts_default.argtypes = [C.POINTER(Opts)]
         L.vc_group_opts_default.argtypes = [C.POINTER(GroupOpts)]
         _lib = L
@@ -200,6 +203,12 @@ def vc_attn_forward(shape, opts, inp: PreppedBuffers, q_perm, O, stream=None):
                                                     _ptr(O), _stream(stream)))
 
 
+def vc_attn_forward_codes(shape, opts, inp: PreppedBuffers, q_perm, O, p_codes, stream=None):
+    st = inp.as_struct()
+    _check("vc_attn_forward_codes", lib().vc_attn_forward_codes(C.byref(shape), C.byref(opts), C.byref(st),
+                                                                _ptr(q_perm), _ptr(O), _ptr(p_codes), _stream(stream)))
+
+
 class Attention:
     """Buffers for one attention shape and the three calls of the path.
 
@@ -242,3 +251,7 @@ class Attention:
 
     def forward(self, O, q_perm=None, stream=None):
         vc_attn_forward(self.shape, self.opts, self.prepped, q_perm, O, stream)
+
+    def forward_codes(self, O, p_codes, q_perm=None, stream=None):
+        """forward() that also writes the probability codes, uint8 [B, H, N, 128 T] (debugging)."""
+        vc_attn_forward_codes(self.shape, self.opts, self.prepped, q_perm, O, p_codes, stream)

@@ -253,8 +253,8 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   return hip_status(vc::launch_prep(a, (int)BH, static_cast<hipStream_t>(stream)));
 }
 
-vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in, const int32_t* q_perm,
-                          uint16_t* O, void* stream) {
+static vc_status attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in, const int32_t* q_perm,
+                              uint16_t* O, uint8_t* p_codes, void* stream) {
   vc_status st = check_shape(shape);
   if (st != VC_OK) return st;
   if ((st = check_opts(opts)) != VC_OK) return st;
@@ -267,6 +267,7 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
   for (const void* p : ptrs)
     if (!aligned16(p)) return VC_ERR_ALIGN;
   if (q_perm && !aligned16(q_perm)) return VC_ERR_ALIGN;
+  if (p_codes && !aligned16(p_codes)) return VC_ERR_ALIGN;
 
   vc::FwdArgs a{};
   const size_t BH = (size_t)shape->B * shape->H;
@@ -279,6 +280,7 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
   a.v_mean = in->v_mean;
   a.q_perm = q_perm;
   a.O = O;
+  a.p_codes = p_codes;
   a.N = shape->N;
   a.T = blocks_of(shape->N, 128);
   // score scale in log2 units: sm_scale * log2(e), with the unnormalised Hadamard's 1/128
@@ -293,6 +295,17 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
   a.q_mxs = in->q_mx_scale;
   a.k_mxs = in->k_mx_scale;
   return hip_status(vc::launch_forward(a, (int)BH, static_cast<hipStream_t>(stream)));
+}
+
+vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in, const int32_t* q_perm,
+                          uint16_t* O, void* stream) {
+  return attn_forward(shape, opts, in, q_perm, O, nullptr, stream);
+}
+
+vc_status vc_attn_forward_codes(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in,
+                                const int32_t* q_perm, uint16_t* O, uint8_t* p_codes, void* stream) {
+  if (!p_codes) return VC_ERR_NULL;
+  return attn_forward(shape, opts, in, q_perm, O, p_codes, stream);
 }
 
 const char* vc_status_str(vc_status s) {

@@ -183,7 +183,9 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
-template <int PMODE, int QKF>
+// DUMP: also write the probability codes of every tile to a.p_codes (a debugging variant; the
+// stores wait for all copies in flight, so it runs unpipelined)
+template <int PMODE, int QKF, bool DUMP>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_fwd(FwdArgs a) {
   constexpr bool I8 = QKF == VC_QK_INT8, F8 = QKF == VC_QK_FP8, MX = QKF == VC_QK_MXFP4;
   using SV = std::conditional_t<I8, v16i, v16f>;  // a lane's 16 scores of one 32-key block
@@ -474,6 +476,23 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     pin(m_run);
     pin(ksc);
   };
+  // codes of tile j (in pc) into row q of a.p_codes, dword w of chunk kc = keys 32(2kc + w/4) +
+  // 8(w%4) + 4kh .. +3; then every copy in flight and these stores complete, which leaves the
+  // copy counting of the schedule as it is
+  const int q_dump = qt * NQ + wave * 32 + col;
+  auto dump_codes = [&](int j) __attribute__((always_inline)) {
+    if constexpr (DUMP) {
+      if (q_dump < a.N) {
+        uint8_t* row = a.p_codes + ((size_t)bh * a.N + q_dump) * ((size_t)T * BLK) + (size_t)j * BLK + 4 * kh;
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+          for (int w = 0; w < 8; ++w)
+            *reinterpret_cast<int*>(row + 32 * (2 * kc + (w >> 2)) + 8 * (w & 3)) = pc[kc][w];
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+  };
   auto end_iter = [&](int npairs) __attribute__((always_inline)) {
     pin_state();
     wait_pairs(npairs);
@@ -487,6 +506,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   auto iter = [&](auto COPYC, auto SOFTC, auto QKC, auto MASKC, auto LASTC, int j, const uint8_t* vt,
                   const uint8_t* kt, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
     constexpr bool cp = decltype(COPYC)::value, soft = decltype(SOFTC)::value, doqk = decltype(QKC)::value;
+    dump_codes(j);
     v8i vop[8];
 #pragma unroll
     for (int n = 0; n < 8; ++n) vop[n] = load_vop(vt, n);
@@ -532,6 +552,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   auto fence = []() __attribute__((always_inline)) { __builtin_amdgcn_sched_barrier(0); };
   auto iter_fast = [&](auto COPYC, int j, const uint8_t* vt, const uint8_t* kt, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
     constexpr bool cp = decltype(COPYC)::value;
+    dump_codes(j);
     auto hook = [&](int k) __attribute__((always_inline)) {
       if (cp && k < PAIR_COPIES) load_part(k, j + 3, kd, vd);
     };
@@ -768,14 +789,24 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
 
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s) {
   const dim3 grid((a.N + NQ - 1) / NQ, BH);
-  auto go = [&](auto PC) {
+  auto go = [&](auto PC, auto DC) {
     constexpr int pm = decltype(PC)::value;
-    if (a.qk_fmt == VC_QK_MXFP4) attn_fwd<pm, VC_QK_MXFP4><<<grid, NTH, 0, s>>>(a);
-    else if (a.qk_fmt == VC_QK_FP8) attn_fwd<pm, VC_QK_FP8><<<grid, NTH, 0, s>>>(a);
-    else attn_fwd<pm, VC_QK_INT8><<<grid, NTH, 0, s>>>(a);
+    constexpr bool dump = decltype(DC)::value;
+    if (a.qk_fmt == VC_QK_MXFP4) attn_fwd<pm, VC_QK_MXFP4, dump><<<grid, NTH, 0, s>>>(a);
+    else if (a.qk_fmt == VC_QK_FP8) attn_fwd<pm, VC_QK_FP8, dump><<<grid, NTH, 0, s>>>(a);
+    else attn_fwd<pm, VC_QK_INT8, dump><<<grid, NTH, 0, s>>>(a);
   };
-  if (a.p_mode == 0) go(std::integral_constant<int, 0>{});
-  else go(std::integral_constant<int, 1>{});
+  const std::integral_constant<int, 0> EXPCAST;
+  const std::integral_constant<int, 1> EXPTHENCAST;
+  const std::integral_constant<bool, true> DUMP;
+  const std::integral_constant<bool, false> NODUMP;
+  if (a.p_codes) {
+    if (a.p_mode == 0) go(EXPCAST, DUMP);
+    else go(EXPTHENCAST, DUMP);
+  } else {
+    if (a.p_mode == 0) go(EXPCAST, NODUMP);
+    else go(EXPTHENCAST, NODUMP);
+  }
   return hipGetLastError();
 }
 

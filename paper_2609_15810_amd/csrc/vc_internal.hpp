@@ -40,6 +40,7 @@ struct FwdArgs {
   const uint8_t *q_mxs, *k_mxs;  // E8M0 scale bytes (MXFP4 only)
   const int32_t* q_perm;
   uint16_t* O;
+  uint8_t* p_codes;  // debugging: the probability codes of every tile [B*H][N][128 T], or null
   int N, T;
   float kappa;      // sm_scale * log2(e) (/ 128 with the Hadamard rotation), rounded once to fp32
   float cbias;      // fl(120 + beta)

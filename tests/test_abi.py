@@ -92,6 +92,12 @@ def test_forward_and_group_validation(L):
     assert L.vc_attn_forward(C.byref(shape()), C.byref(mx), C.byref(P), FAKE, FAKE, None) == 1
     P10 = vc.Prepped(*([FAKE] * 10)); P10.q_scale = P10.k_scale = None; P10.q_mx_scale = FAKE + 4
     assert L.vc_attn_forward(C.byref(shape()), C.byref(mx), C.byref(P10), FAKE, FAKE, None) == 5
+    # the code-dumping variant: same checks, and the code buffer is required and aligned
+    fc = L.vc_attn_forward_codes
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, None, None) == 1
+    assert fc(C.byref(shape(Wd=15)), C.byref(o), C.byref(P), None, FAKE, FAKE, None) == 2
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, None, FAKE, None) == 1
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, FAKE + 4, None) == 5
     g = vc.make_group_opts(k=65)
     assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 3
     g = vc.make_group_opts(iters=-1)
