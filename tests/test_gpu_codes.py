@@ -24,7 +24,7 @@ import synthetic as S
 torch = pytest.importorskip("torch")
 vc = pytest.importorskip("paper_2609_15810_amd")
 
-from test_gpu_parity import dev16, dev32  # noqa: E402
+from test_gpu_parity import check_output, dev16, dev32  # noqa: E402
 from test_gpu_mx import rand_qkv  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -96,6 +96,23 @@ def test_expcast_int8_codes_tile_counts(N):
     rows = np.arange(0, N, 1 if N <= 1100 else 7)
     o = oracle.attention_codes(oracle_pp(Q, K, V, (1, 1, N)), rows)
     assert_codes_equal(g, o, rows, f"N={N}")
+    assert np.array_equal(O1, O2)
+
+
+@pytest.mark.parametrize("sm_scale,beta", [(0.05, -0.35), (0.125, 0.0), (0.0625, -0.5)])
+def test_expcast_int8_codes_softmax_scale_and_beta(sm_scale, beta):
+    """Non-default softmax scale and ExpCast shift: codes bit-exact and the output within the
+    tolerance of the oracle's pipeline with the same options."""
+    Q, K, V = rand_qkv(1, 2, 1000, 101)
+    grid, perm = (5, 8, 25), S.random_perm(1000, 102, 1, 2)
+    g, O1, O2 = gpu_codes(Q, K, V, grid, perm, sm_scale=sm_scale, beta=beta)
+    pp = oracle_pp(Q, K, V, grid, perm)
+    rows = np.arange(1000)
+    o = oracle.attention_codes(pp, rows, sm_scale=sm_scale, beta=beta)
+    assert_codes_equal(g, o, rows, f"sm_scale={sm_scale} beta={beta}")
+    ref = oracle.attention(pp, rows, sm_scale=sm_scale, beta=beta)
+    check_output(S.bits_to_f32(O2.view(np.uint16)).reshape(2, 1000, 128).astype(np.float64), ref,
+                 f"sm_scale={sm_scale} beta={beta}")
     assert np.array_equal(O1, O2)
 
 
