@@ -548,11 +548,16 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   // steady-state iteration j (codes of tile j+1 and scores of tile j+2 exist, neither is the last
   // tile), issued in regions that each pair matrix work with vector work of about the same
   // length; the scheduling barriers keep the regions in this order, so the scores of key block
-  // kb of tile j+2 are written only after the codes of key block kb of tile j+1 are formed
+  // kb of tile j+2 are written only after the codes of key block kb of tile j+1 are formed.
+  // The wave's issue priority steps down from 3 to 0 over the regions: of the two waves sharing a
+  // SIMD, the one further behind in the iteration wins the arbitration, so both reach the
+  // barrier together (with equal priorities the older wave runs ahead and the other finishes the
+  // iteration alone, without a partner to overlap its matrix and vector work)
   auto fence = []() __attribute__((always_inline)) { __builtin_amdgcn_sched_barrier(0); };
   auto iter_fast = [&](auto COPYC, int j, const uint8_t* vt, const uint8_t* kt, uint8_t* kd, uint8_t* vd) __attribute__((always_inline)) {
     constexpr bool cp = decltype(COPYC)::value;
     dump_codes(j);
+    __builtin_amdgcn_s_setprio(3);
     auto hook = [&](int k) __attribute__((always_inline)) {
       if (cp && k < PAIR_COPIES) load_part(k, j + 3, kd, vd);
     };
@@ -633,6 +638,8 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     pin(mk0);
     pin(mk1);
     fence();
+    __builtin_amdgcn_s_setprio(2);
+    fence();
     // R2: value products 2, 3; operands 4, 5; maxima of blocks 2, 3, m', alpha
     o[2] = mfma_f8(vb[0], pc[0], o[2]);
     o[3] = mfma_f8(vb[1], pc[0], o[3]);
@@ -661,6 +668,8 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     codes_kb(0);
     hook(2);
     fence();
+    __builtin_amdgcn_s_setprio(1);
+    fence();
     // R4: value products 6, 7, scores of block 0; key operands of block 1; codes of block 1
     load_kops(0, k0);
     o[2] = mfma_f8(vb[0], pc[1], o[2]);
@@ -675,6 +684,8 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     load_kops(2, k0);
     codes_kb(2);
     hook(4);
+    fence();
+    __builtin_amdgcn_s_setprio(0);
     fence();
     // R6: scores of block 2; key operands of block 3; codes of block 3
     qk_kb(std::integral_constant<int, 2>{}, k0);
@@ -749,6 +760,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
       }
     }
   }
+  __builtin_amdgcn_s_setprio(0);
   auto kbuf = [&](int b) __attribute__((always_inline)) -> const uint8_t* {
     return b == 0 ? kb0 : (b == 1 ? kb1 : (b == 2 ? kb2 : kb3));
   };
