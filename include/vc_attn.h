@@ -222,13 +222,15 @@ vc_status vc_attn_forward(const vc_shape *shape, const vc_opts *opts, const vc_p
  * direct-fp8 in ExpCast mode, the FP8 cast of the exponentials otherwise), for debugging and
  * parity checks; it waits for every tile copy in flight before each tile, so copies no longer
  * overlap the computation.
- *   p_codes : device uint8 [B, H, N, 128 T] (T = ceil(N / 128)), 16-byte aligned, caller-owned,
- *             fully overwritten. Row i is the prepared query i (before q_perm); byte 128 t + s is
- *             key s of tile t of the prepared K', coded at the running maximum after tile t;
- *             keys past N are 0.
+ *   p_codes       : device uint8 [B, H, N, 128 T] (T = ceil(N / 128)), 16-byte aligned,
+ *                   caller-owned, fully overwritten. Row i is the prepared query i (before q_perm);
+ *                   byte 128 t + s is key s of tile t of the prepared K', coded at the running
+ *                   maximum after tile t; keys past N are 0.
+ *   p_codes_bytes : size of the p_codes buffer; VC_ERR_WORKSPACE if below B*H*N*128*T.
  * Other arguments and errors as vc_attn_forward; VC_ERR_NULL if p_codes is NULL. */
 vc_status vc_attn_forward_codes(const vc_shape *shape, const vc_opts *opts, const vc_prepped *in,
-                                const int32_t *q_perm, uint16_t *O, uint8_t *p_codes, void *stream);
+                                const int32_t *q_perm, uint16_t *O, uint8_t *p_codes,
+                                size_t p_codes_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *vc_status_str(vc_status s);

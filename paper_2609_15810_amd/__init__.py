@@ -85,7 +85,7 @@ def lib():
                                       C.c_void_p, C.c_void_p]
         L.vc_attn_forward_codes.restype = C.c_int
         L.vc_attn_forward_codes.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.POINTER(Prepped), C.c_void_p,
-                                            C.c_void_p, C.c_void_p, C.c_void_p]
+                                            C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
         L.vc_opts_default.argtypes = [C.POINTER(Opts)]
         L.vc_group_opts_default.argtypes = [C.POINTER(GroupOpts)]
         _lib = L
@@ -205,8 +205,10 @@ def vc_attn_forward(shape, opts, inp: PreppedBuffers, q_perm, O, stream=None):
 
 def vc_attn_forward_codes(shape, opts, inp: PreppedBuffers, q_perm, O, p_codes, stream=None):
     st = inp.as_struct()
+    nbytes = p_codes.numel() * p_codes.element_size() if p_codes is not None else 0
     _check("vc_attn_forward_codes", lib().vc_attn_forward_codes(C.byref(shape), C.byref(opts), C.byref(st),
-                                                                _ptr(q_perm), _ptr(O), _ptr(p_codes), _stream(stream)))
+                                                                _ptr(q_perm), _ptr(O), _ptr(p_codes), nbytes,
+                                                                _stream(stream)))
 
 
 class Attention:

@@ -303,8 +303,13 @@ vc_status vc_attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_p
 }
 
 vc_status vc_attn_forward_codes(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in,
-                                const int32_t* q_perm, uint16_t* O, uint8_t* p_codes, void* stream) {
+                                const int32_t* q_perm, uint16_t* O, uint8_t* p_codes, size_t p_codes_bytes,
+                                void* stream) {
+  const vc_status st = check_shape(shape);
+  if (st != VC_OK) return st;
   if (!p_codes) return VC_ERR_NULL;
+  const size_t need = (size_t)shape->B * shape->H * shape->N * ((size_t)blocks_of(shape->N, 128) * 128);
+  if (p_codes_bytes < need) return VC_ERR_WORKSPACE;
   return attn_forward(shape, opts, in, q_perm, O, p_codes, stream);
 }
 

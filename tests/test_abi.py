@@ -94,10 +94,12 @@ def test_forward_and_group_validation(L):
     assert L.vc_attn_forward(C.byref(shape()), C.byref(mx), C.byref(P10), FAKE, FAKE, None) == 5
     # the code-dumping variant: same checks, and the code buffer is required and aligned
     fc = L.vc_attn_forward_codes
-    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, None, None) == 1
-    assert fc(C.byref(shape(Wd=15)), C.byref(o), C.byref(P), None, FAKE, FAKE, None) == 2
-    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, None, FAKE, None) == 1
-    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, FAKE + 4, None) == 5
+    need = 2 * 1024 * 1024   # B*H*N*128*T for the 2-head, 1024-token shape
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, None, need, None) == 1
+    assert fc(C.byref(shape(Wd=15)), C.byref(o), C.byref(P), None, FAKE, FAKE, need, None) == 2
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, FAKE, need - 1, None) == 4
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, None, FAKE, need, None) == 1
+    assert fc(C.byref(shape()), C.byref(o), C.byref(P), None, FAKE, FAKE + 4, need, None) == 5
     g = vc.make_group_opts(k=65)
     assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == 3
     g = vc.make_group_opts(iters=-1)
