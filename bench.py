@@ -78,13 +78,14 @@ def measured_traffic():
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=512):
-    """Time the oracle (never tuned) on a bounded sample, and compare the GPU output there."""
+def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=1536):
+    """Time the oracle (never tuned) on a bounded sample, and compare the GPU output there: whole
+    query blocks spread evenly over the head, the first and the ragged last among them."""
     import oracle
     H = Q.shape[1]
     N = Q.shape[2]
     T = (N + 127) // 128
-    blocks = sorted({0, T // 3, (2 * T) // 3, T - 1})[: max(1, rows_per_head // 128)]
+    blocks = sorted({int(b) for b in np.linspace(0, T - 1, max(1, min(T, rows_per_head // 128))).round()})
     rows = np.concatenate([np.arange(128 * b, min(N, 128 * b + 128)) for b in blocks]).astype(np.int32)
     t0 = time.perf_counter()
     g = oracle.group(V, grid, k=32, iters=8)
