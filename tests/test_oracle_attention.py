@@ -52,12 +52,24 @@ def closed_form(pp, h, i, sm_scale, beta=-0.35):
     sv = pp["v_scale"].reshape(-1, 128)[h].astype(np.float64)
     mu = S.bits_to_f32(pp["v_mean"].reshape(-1, T, 128)[h]).astype(np.float64)
     kappa = np.float32(sm_scale * np.log2(np.e) / (128.0 if pp["hadamard"] else 1.0))
-    if pp.get("qk_fmt", 0) == oracle.QK_FP8:
-        # E4M3 codes: exact fp64 dot products of the decoded values, rounded once to fp32
-        acc = (_decode(kc) @ _decode(q)).astype(np.float32)
+    fmt = pp.get("qk_fmt", 0)
+    if fmt == oracle.QK_MXFP4:
+        # E2M1 elements times 2^(byte - 127) per 32-channel block, from the OCP MX tables; the
+        # block scales are inside the score, whose scale is kappa alone
+        e2m1 = np.array([0, .5, 1, 1.5, 2, 3, 4, 6, 0, -.5, -1, -1.5, -2, -3, -4, -6])
+        qd = e2m1[pp["q_mx"].reshape(-1, T * 128, 128)[h, i]] * np.repeat(
+            np.exp2(pp["q_mxs"].reshape(-1, T * 128, 4)[h, i].astype(np.float64) - 127), 32)
+        kd = e2m1[pp["k_mx"].reshape(-1, T * 128, 128)[h, :N]] * np.repeat(
+            np.exp2(pp["k_mxs"].reshape(-1, T * 128, 4)[h, :N].astype(np.float64) - 127), 32, axis=1)
+        acc = (kd @ qd).astype(np.float32)
+        a = np.full(T, kappa, np.float32)
     else:
-        acc = kc.astype(np.int64) @ q.astype(np.int64)      # exact int64 dot products
-    a = np.array([np.float32(np.float32(sq * ks[j]) * kappa) for j in range(T)], np.float32)
+        if fmt == oracle.QK_FP8:
+            # E4M3 codes: exact fp64 dot products of the decoded values, rounded once to fp32
+            acc = (_decode(kc) @ _decode(q)).astype(np.float32)
+        else:
+            acc = kc.astype(np.int64) @ q.astype(np.int64)      # exact int64 dot products
+        a = np.array([np.float32(np.float32(sq * ks[j]) * kappa) for j in range(T)], np.float32)
     tmax = np.array([np.float32(np.float32(acc[128 * j:128 * (j + 1)].max()) * a[j]) for j in range(T)], np.float32)
     m = np.maximum.accumulate(tmax)                         # running maximum after each tile
     num = np.zeros(128)

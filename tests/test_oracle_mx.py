@@ -128,3 +128,25 @@ def test_mx_attention_close_to_exact():
     oi = oracle.attention(pi, rows)
     rel_i = np.linalg.norm(oi - exact) / np.linalg.norm(exact)
     assert rel < 0.1 and rel_i < rel, (rel, rel_i)
+
+
+@pytest.mark.parametrize("grid,hadamard,smooth_v", [((5, 8, 25), True, True), ((3, 5, 7), False, False)])
+def test_mx_attention_matches_closed_form(grid, hadamard, smooth_v):
+    """The recurrence against the non-recurrent closed form with scores as exact dot products of
+    the blocks dequantized from the OCP tables (E2M1 value times 2^(byte - 127)), rounded once to
+    fp32, and score scale kappa (R21)."""
+    from test_oracle_attention import closed_form
+    rng = np.random.default_rng(sum(grid) + 3)
+    N = grid[0] * grid[1] * grid[2]
+    Q = S.bf16_bits(rng.standard_normal((1, 2, N, 128)).astype(np.float32) * 2)
+    K = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * 2 + rng.standard_normal(128) * 3).astype(np.float32))
+    V = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) + rng.standard_normal(128) * 2).astype(np.float32))
+    pp = oracle.prep(Q, K, V, grid, perm=S.random_perm(N, 2, 1, 2), hadamard=hadamard, smooth_v=smooth_v,
+                     qk_fmt=oracle.QK_MXFP4)
+    rows = np.unique(np.concatenate([np.arange(0, N, max(1, N // 9)), [N - 1]])).astype(np.int32)
+    sm = float(np.float32(1 / np.sqrt(128)))
+    ours = oracle.attention(pp, rows, sm_scale=sm)
+    for h in range(2):
+        for t, i in enumerate(rows):
+            ref = closed_form(pp, h, int(i), sm)
+            assert np.abs(ours[h, t] - ref).max() <= 1e-9 * (1 + np.abs(ref).max())
