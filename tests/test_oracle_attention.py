@@ -40,8 +40,9 @@ def _decode(b):
     return torch.from_numpy(np.ascontiguousarray(b, np.uint8)).view(torch.float8_e4m3fn).double().numpy()
 
 
-def closed_form(pp, h, i, sm_scale, beta=-0.35):
-    """Non-recurrent evaluation of the quantized pipeline for query row i of head h."""
+def closed_form(pp, h, i, sm_scale, beta=-0.35, p_mode=oracle.P_EXPCAST):
+    """Non-recurrent evaluation of the quantized pipeline for query row i of head h (ExpCast codes,
+    or with p_mode = exponentiate-then-cast the torch E4M3 cast of 256 exp2(fl(fl(s a) - m')))."""
     N = pp["N"]
     T = (N + 127) // 128
     q = pp["q"].reshape(-1, T * 128, 128)[h, i]
@@ -76,15 +77,40 @@ def closed_form(pp, h, i, sm_scale, beta=-0.35):
     den = 0.0
     for j in range(T):
         sl = slice(128 * j, min(128 * (j + 1), N))
-        bias = np.float32(np.float32(np.float32(120.0) + np.float32(beta)) - np.float32(8.0) * m[j])
-        c = np.float32(acc[sl].astype(np.float64) * (8.0 * np.float64(a[j])) + np.float64(bias))
-        code = np.clip(np.rint(c), 0, 120).astype(np.uint8)
+        if p_mode == oracle.P_EXPCAST:
+            bias = np.float32(np.float32(np.float32(120.0) + np.float32(beta)) - np.float32(8.0) * m[j])
+            c = np.float32(acc[sl].astype(np.float64) * (8.0 * np.float64(a[j])) + np.float64(bias))
+            code = np.clip(np.rint(c), 0, 120).astype(np.uint8)
+        else:
+            u = (acc[sl].astype(np.float32) * a[j]).astype(np.float32) - m[j]
+            pe = np.exp2(u.astype(np.float64)).astype(np.float32) * np.float32(256.0)
+            code = torch.from_numpy(pe.astype(np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
         p = _decode(code)
         w = 2.0 ** (float(m[j]) - float(m[-1]))             # one rescale from tile j to the end
         mu_code = mu[j] / sv if pp["smooth_v"] else 0.0
         num += w * (p @ vd[sl] + p.sum() * mu_code)
         den += w * p.sum()
     return num * sv / den
+
+
+@pytest.mark.parametrize("qk_fmt", [oracle.QK_INT8, oracle.QK_FP8, oracle.QK_MXFP4])
+def test_exp_then_cast_attention_matches_closed_form(qk_fmt):
+    """The exponentiate-then-cast recurrence against the closed form (exp2 in fp64 rounded once,
+    then the library's E4M3 cast), for every score format."""
+    grid = (5, 8, 25)
+    rng = np.random.default_rng(77 + qk_fmt)
+    N = grid[0] * grid[1] * grid[2]
+    Q = S.bf16_bits(rng.standard_normal((1, 2, N, 128)).astype(np.float32) * 2)
+    K = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * 2 + rng.standard_normal(128) * 3).astype(np.float32))
+    V = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) + rng.standard_normal(128) * 2).astype(np.float32))
+    pp = oracle.prep(Q, K, V, grid, perm=S.random_perm(N, 5, 1, 2), qk_fmt=qk_fmt)
+    rows = np.unique(np.concatenate([np.arange(0, N, max(1, N // 9)), [N - 1]])).astype(np.int32)
+    sm = float(np.float32(1 / np.sqrt(128)))
+    ours = oracle.attention(pp, rows, sm_scale=sm, p_mode=oracle.P_EXP_THEN_CAST)
+    for h in range(2):
+        for t, i in enumerate(rows):
+            ref = closed_form(pp, h, int(i), sm, p_mode=oracle.P_EXP_THEN_CAST)
+            assert np.abs(ours[h, t] - ref).max() <= 1e-9 * (1 + np.abs(ref).max())
 
 
 @pytest.mark.parametrize("grid,hadamard,smooth_v", [((5, 8, 25), True, True), ((4, 16, 16), True, True),
