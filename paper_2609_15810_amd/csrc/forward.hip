@@ -56,6 +56,7 @@
 namespace vc {
 
 constexpr int NW = 8;             // waves per workgroup, 32 queries each (two per SIMD)
+constexpr int NXCD = 8;           // accelerator complex dies (each with its own L2)
 constexpr int NTH = 64 * NW;
 constexpr int NQ = 32 * NW;
 constexpr int TILE_BYTES = BLK * D;
@@ -204,7 +205,19 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   __shared__ __attribute__((aligned(16))) float2 rm[NW][32][8];
   __shared__ float svs[D], inv_svs[D];
 
-  const int qt = blockIdx.x, bh = blockIdx.y;
+  // The dispatcher deals workgroups to the XCDs round-robin by linear id; the remap (a bijection
+  // when the count divides evenly) gives each XCD a contiguous range of (head, query tile) pairs,
+  // so its L2 serves one or two heads' K/V tiles instead of every head's (half the HBM fetches;
+  // the time is unchanged, the kernel is not memory-bound)
+  int qt = blockIdx.x, bh = blockIdx.y;
+  {
+    const int total = gridDim.x * gridDim.y, id = blockIdx.x + gridDim.x * blockIdx.y;
+    if (total % NXCD == 0) {
+      const int l = (id % NXCD) * (total / NXCD) + id / NXCD;
+      qt = l % gridDim.x;
+      bh = l / gridDim.x;
+    }
+  }
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kh = lane >> 5, col = lane & 31;
