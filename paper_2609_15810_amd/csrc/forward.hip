@@ -192,7 +192,8 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   using SV = std::conditional_t<I8, v16i, v16f>;  // a lane's 16 scores of one 32-key block
   using QO = std::conditional_t<F8, v8i, v4i>;    // one Q or K operand of the score product
   // K_t in kb[t % 4] (MXFP4: codes, then scale bytes at MX_CODE_BYTES); V_t with its 128 bf16 block means in vb[t % 4]; mu_t / s_V as bf16 hi + lo
-  // in slot t % 8 of ub[(t / 8) % 2]; (r_t, m_t) per query in slot t % 8 of rm[wave]
+  // in slot t % 8 of ub[(t / 8) % 2]; (r_t, m_t) per query in slot t % 8 of rm[wave] (slot-major, so
+  // that a wave's 32 queries write and read 32 consecutive 8-byte words: no bank conflicts)
   __shared__ __attribute__((aligned(16))) uint8_t kb0[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t kb1[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t kb2[TILE_BYTES];
@@ -202,7 +203,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   __shared__ __attribute__((aligned(16))) uint8_t vb2[VBUF_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t vb3[VBUF_BYTES];
   __shared__ __attribute__((aligned(16))) uint16_t ub[2][2][D][8];
-  __shared__ __attribute__((aligned(16))) float2 rm[NW][32][8];
+  __shared__ __attribute__((aligned(16))) float2 rm[NW][8][32];
   __shared__ float svs[D], inv_svs[D];
 
   // The dispatcher deals workgroups to the XCDs round-robin by linear id; the remap (a bijection
@@ -336,14 +337,14 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   SV s[4];         // scores of the tile whose codes are computed next
   v8i pc[2];       // codes of the tile whose value product is issued next
   float ksc = 0.f;  // scale of the K tile whose scores are in s
-  float2* rm_q = &rm[wave][col][0];
+  float2* rm_q = &rm[wave][0][col];   // slot t at rm_q[32 t]
 
   // O^T += M^T R for the tiles of chunk parity `par` whose slot is <= last_slot, R_t = r_t 2^(m_t - m)
   auto flush_means = [&](int par, int last_slot) __attribute__((always_inline)) {
     bf16x8 b;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      const float2 e = rm_q[t];
+      const float2 e = rm_q[32 * t];
       const float R = t <= last_slot ? e.x * __builtin_amdgcn_exp2f(e.y - m_run) : 0.f;
       const uint16_t hi = f32_to_bf16(R);
       const uint16_t v = kh == 0 ? hi : f32_to_bf16(R - bf16_to_f32(hi));
@@ -540,7 +541,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     if (doqk) qk(MASKC, j + 2, kt);
     const float rsum = rs[0];
     if (a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
-    rm_q[j & 7] = make_float2(rsum, m_run);
+    rm_q[32 * (j & 7)] = make_float2(rsum, m_run);
     l_run += rsum;
     if (tid < D) stash_mean(j, vt);
     if (soft) {
@@ -710,7 +711,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     if (!MX) ksc = kscale[j + 2];
     const float rsum = rs[0];
     if (a.smooth_v && j >= 8 && (j & 7) == 0) flush_means(((j >> 3) - 1) & 1, 7);
-    rm_q[j & 7] = make_float2(rsum, m_run);
+    rm_q[32 * (j & 7)] = make_float2(rsum, m_run);
     l_run += rsum;
     if (tid < D) stash_mean(j, vt);
     if (__builtin_amdgcn_ballot_w64(alpha_p != 1.f)) {
