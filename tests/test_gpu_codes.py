@@ -87,10 +87,11 @@ def test_expcast_int8_codes_bit_exact(case):
     assert np.array_equal(O1, O2), "the dumping variant changed the output"
 
 
-@pytest.mark.parametrize("N", [1, 100, 300, 500, 700, 833, 1100, 1400, 1900, 2500])
+@pytest.mark.parametrize("N", [1, 100, 129, 257, 300, 385, 500, 513, 700, 833, 1100, 1400, 1900, 2500])
 def test_expcast_int8_codes_tile_counts(N):
-    """Tile counts 1..11 and 20 with ragged last tiles: the prologue, every remainder of the
-    four-way unrolled loop and the tail iterations each form some of the codes."""
+    """Tile counts 1..11 and 20 with ragged last tiles, among them last tiles holding a single key
+    (N = 129, 257, 385, 513: 127 padded keys masked): the prologue, every remainder of the four-way
+    unrolled loop and the tail iterations each form some of the codes."""
     Q, K, V = rand_qkv(1, 2, N, 300 + N)
     g, O1, O2 = gpu_codes(Q, K, V, (1, 1, N))
     rows = np.arange(0, N, 1 if N <= 1100 else 7)
