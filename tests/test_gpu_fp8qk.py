@@ -225,7 +225,7 @@ def test_forward_f8_ragged_perm(flags):
         check_output_f8(o[h][qp[0, h]], ref_prepared[h], bound, "fp8 " + str(flags) + f" head {h}")
 
 
-@pytest.mark.parametrize("N", [1, 100, 300, 500, 700, 833, 1100, 1400, 1900, 2500])
+@pytest.mark.parametrize("N", [1, 100, 129, 300, 500, 513, 700, 833, 1100, 1400, 1900, 2500])
 def test_forward_f8_tile_counts(N):
     """Tile counts 1..11 and 20 with ragged last tiles: every remainder of the unrolled tile loop."""
     Q, K, V = rand_qkv(1, 2, N, 400 + N)

@@ -147,7 +147,7 @@ def test_forward_mx_ragged_perm(flags):
     check_output(o.reshape(2, 1000, 128), ref, "mx " + str(flags))
 
 
-@pytest.mark.parametrize("N", [1, 100, 300, 500, 700, 833, 1100, 1400, 1900, 2500])
+@pytest.mark.parametrize("N", [1, 100, 129, 300, 500, 513, 700, 833, 1100, 1400, 1900, 2500])
 def test_forward_mx_tile_counts(N):
     """Tile counts 1..11 and 20 with ragged last tiles: every remainder of the unrolled tile loop."""
     Q, K, V = rand_qkv(1, 2, N, 200 + N)

@@ -173,7 +173,7 @@ def test_forward_ragged_perm(flags):
     check_output(o.reshape(2, 1000, 128), ref, str(flags))
 
 
-@pytest.mark.parametrize("N", [1, 100, 200, 300, 500, 600, 700, 833, 1100, 1280, 1400, 1900, 2100, 2500])
+@pytest.mark.parametrize("N", [1, 100, 129, 200, 257, 300, 500, 513, 600, 700, 833, 1100, 1280, 1400, 1900, 2100, 2500])
 def test_forward_tile_counts(N):
     """Every key-tile count from 1 to 11 and 17 (so every remainder of the tile loop, mean batches
     of 8 that end full or partial) with a ragged last tile where N is not a multiple of 128."""
