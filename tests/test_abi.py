@@ -61,6 +61,9 @@ def test_prep_validation(L):
     assert prep_call(L, shape(d=64), o) == 2
     assert prep_call(L, shape(N=1000), o) == 2
     assert prep_call(L, shape(B=0), o) == 2
+    assert prep_call(L, shape(H=0), o) == 2
+    assert prep_call(L, shape(N=0, F=0), o) == 2          # empty token grid
+    assert prep_call(L, shape(H=128, N=131072, F=32, Ht=64, Wd=64), o) == 2   # B*H*Np*128 reaches 2^31
     bad = vc.make_opts(); bad.p_mode = 7
     assert prep_call(L, shape(), bad) == 3
     bad = vc.make_opts(); bad.smooth_v = 2
