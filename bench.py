@@ -101,6 +101,7 @@ def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=1536):
     o = O_gpu[:, rows].astype(np.float64)
     err = o - o_ref
     half_ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(o_ref), 1e-30))) - 8)
+    ulps = bf16_ulp_distance(S_bits(o), oracle.bf16_round(o_ref.astype(np.float32)))
     cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
     return dict(
         baseline=dict(value=ops / t_step_est / 1e12, unit="TOPS", cores=cores, kind="oracle",
@@ -111,9 +112,35 @@ def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=1536):
                     rel_l2_vs_oracle=float(np.linalg.norm(err) / np.linalg.norm(o_ref)),
                     max_abs_vs_oracle=float(np.abs(err).max()),
                     max_abs_excess_over_bf16_half_ulp=float((np.abs(err) - half_ulp).max()),
+                    frac_bf16_equal_to_oracle_bf16=float((ulps == 0).mean()),
+                    frac_bf16_within_1ulp_of_oracle_bf16=float((ulps <= 1).mean()),
+                    max_bf16_ulp_vs_oracle_bf16=int(ulps.max()),
+                    max_bf16_ulp_vs_oracle_bf16_where_abs_ge_1_16=int(ulps[np.abs(o_ref) >= 0.0625].max()),
                     rel_l2_vs_fp64=float(np.linalg.norm(o - exact) / np.linalg.norm(exact)),
                     psnr_vs_fp64_db=float(10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2))),
                     oracle_rel_l2_vs_fp64=float(np.linalg.norm(o_ref - exact) / np.linalg.norm(exact))))
+
+
+def S_bits(x):
+    """bf16 bit patterns of values that are already bf16 (the GPU output read back)."""
+    b = np.ascontiguousarray(x, np.float32).view(np.uint32)
+    assert not (b & 0xFFFF).any()
+    return (b >> 16).astype(np.uint16)
+
+
+def bf16_ulp_distance(a, b):
+    """|a - b| in bf16 units in the last place, over the ordered bf16 bit patterns."""
+    def ordered(x):
+        x = x.astype(np.int64)
+        mag = x & 0x7FFF
+        return np.where(x & 0x8000, -mag, mag)
+    return np.abs(ordered(a) - ordered(b))
+
+
+def rows_over_gate(o_gpu, o_ref, gate=2e-2):
+    """Rows whose largest error in excess of half a bf16 ulp of the reference exceeds `gate`."""
+    half_ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(o_ref), 1e-30))) - 8)
+    return int(((np.abs(o_gpu - o_ref) - half_ulp).max(axis=-1) > gate).sum())
 
 
 def time_stages(fns, reps):
@@ -275,14 +302,26 @@ def modes_block(vc, S, Qd, Kd, Vd, perm, reps=10):
     return res, (heads, rows, samples)
 
 
-def modes_accuracy(Q, K, V, grid, sample):
-    """rel-L2 and PSNR of each mode's GPU output against exact fp64 attention (oracle)."""
+def modes_accuracy(Q, K, V, grid, sample, perm):
+    """Each mode's GPU output on the sampled rows against the oracle's pipeline in the same mode
+    (rel-L2, and the count of rows over the plain max-abs gate of 2e-2 in excess of half a bf16
+    ulp) and against exact fp64 attention (rel-L2, PSNR)."""
     import oracle
     heads, rows, samples = sample
     exact = oracle.reference_attention(Q[:, heads], K[:, heads], V[:, heads], grid, rows)
-    return {tag: {"rel_l2_vs_fp64": float(np.linalg.norm(o - exact) / np.linalg.norm(exact)),
-                  "psnr_vs_fp64_db": float(10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2)))}
-            for tag, o in samples.items()}
+    pph = {fmt: oracle.prep(Q[:, heads], K[:, heads], V[:, heads], grid, perm=perm[:, heads], qk_fmt=fmt)
+           for fmt in (oracle.QK_INT8, oracle.QK_FP8)}
+    out = {}
+    for tag, o in samples.items():
+        fmt = oracle.QK_FP8 if tag.startswith("fp8") else oracle.QK_INT8
+        pm = oracle.P_EXP_THEN_CAST if tag.endswith("exp_then_cast") else oracle.P_EXPCAST
+        ref = oracle.attention(pph[fmt], rows, p_mode=pm)
+        out[tag] = {"rel_l2_vs_oracle": float(np.linalg.norm(o - ref) / np.linalg.norm(ref)),
+                    "rows_over_2e-2_vs_oracle": rows_over_gate(o, ref),
+                    "rows_compared": int(o.shape[0] * o.shape[1]),
+                    "rel_l2_vs_fp64": float(np.linalg.norm(o - exact) / np.linalg.norm(exact)),
+                    "psnr_vs_fp64_db": float(10 * np.log10(np.abs(exact).max() ** 2 / np.mean((o - exact) ** 2)))}
+    return out
 
 
 def _v_layout_index():
@@ -675,7 +714,7 @@ def main():
         "config": {"workload": f"video-DiT attention layer B={B} H={H} N={N} (grid {grid[0]}x{grid[1]}x{grid[2]}) "
                                f"d=128, grouping k-means k=32 8 rounds, ExpCast-FP8, V-Smooth",
                    "B": B, "H": H, "N": N, "d": 128, "grid": list(grid)},
-        "roofline": {"bound": "mfma", "achieved": attn_tops, "peak": PEAK_8BIT_TOPS, "unit": "TFLOP/s",
+        "roofline": {"bound": "mfma", "achieved": attn_tops, "peak": PEAK_8BIT_TOPS, "unit": "TOPS",
                      "frac": attn_tops / PEAK_8BIT_TOPS, "traffic": traffic},
         "attention": {"kernel": "attn_fwd", "ms_mean": t_attn, "ms_median": t_attn_med, "tops": attn_tops,
                       "frac_8bit_peak": attn_tops / PEAK_8BIT_TOPS},
@@ -701,7 +740,7 @@ def main():
         out["parity"] = r["parity"]
         if not args.no_extra:
             print("[bench] score formats x probability paths: accuracy against fp64", file=sys.stderr, flush=True)
-            for tag, acc in modes_accuracy(Q, K, V, grid, modes_sample).items():
+            for tag, acc in modes_accuracy(Q, K, V, grid, modes_sample, A.perm.cpu().numpy()).items():
                 out["modes"][tag].update(acc)
             print("[bench] 4-bit variant accuracy against fp64", file=sys.stderr, flush=True)
             for tag, acc in mx4_accuracy(mx4_sample).items():

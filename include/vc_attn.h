@@ -85,7 +85,10 @@ enum { VC_P_EXPCAST = 0, VC_P_EXP_THEN_CAST = 1 };
  *   smooth_v : 1 = V-Smooth block demeaning (means restored in the attention kernel);
  *              0 = plain per-channel E4M3 V.
  *   sm_scale : softmax scale; 0 selects 1/sqrt(d).
- *   beta     : ExpCast-FP8 centring constant (the method uses -0.35).
+ *   beta     : ExpCast-FP8 centring constant (the method uses -0.35), -1 <= beta <= 0
+ *              (VC_ERR_UNSUPPORTED otherwise). Sec. 3.3 derives the shift from the rounding
+ *              error range [-0.689, 0]; inside [-1, 0] the row maximum's code stays in
+ *              [119, 120], so no code overflows the clip of eq. direct-fp8 and no row sum is 0.
  * Each flag must be 0 or 1. */
 typedef struct {
     int32_t qk_fmt;
@@ -102,7 +105,7 @@ enum { VC_GROUP_IDENTITY = 0, VC_GROUP_CUBE = 1, VC_GROUP_KMEANS = 2 };
  *                frames x cube[1] rows x cube[2] cols in raster order, tokens in raster order
  *                inside a cube), VC_GROUP_KMEANS (Lloyd k-means on per-head INT8 codes of V,
  *                squared-L2, ties to the smallest cluster; labels sorted stably).
- *   k          : clusters, 1 <= k <= min(N, 256).
+ *   k          : clusters, 1 <= k <= min(N, 64) (VC_ERR_UNSUPPORTED otherwise).
  *   iters      : Lloyd rounds (assign + update), 0 <= iters <= 64.
  *   warm_start : 1 = initialise from `centroids` (value units, previous call's output);
  *                0 = centroid c starts at token floor((2c+1) N / (2k)).
@@ -231,6 +234,21 @@ vc_status vc_attn_forward(const vc_shape *shape, const vc_opts *opts, const vc_p
 vc_status vc_attn_forward_codes(const vc_shape *shape, const vc_opts *opts, const vc_prepped *in,
                                 const int32_t *q_perm, uint16_t *O, uint8_t *p_codes,
                                 size_t p_codes_bytes, void *stream);
+
+/* The FP8 score product of the attention kernel (qk_fmt = VC_QK_FP8, Sec. 4.5), on caller data,
+ * for checking its accumulation error: the kernel forms each 32 keys x 32 queries block of scores
+ * with two chained E4M3 32x32x64 matrix instructions (channels 0..63, then 64..127, the first
+ * result as the second's accumulator input), and this entry point runs that same instruction
+ * sequence from the accumulator c_in:
+ *   out[b][i][j] = c_in[b][i][j] + sum_{c < 128} e4m3(a[b][i][c]) * e4m3(bm[b][j][c]),
+ * summed as the matrix unit sums (not an exact fp32 sum once the products span many binades).
+ *   a, bm : device uint8 [n][32][128], E4M3 (OCP e4m3fn) bytes, row-major.
+ *   c_in  : device fp32 [n][32][32], the accumulator input (zeros reproduce the kernel's scores).
+ *   out   : device fp32 [n][32][32].
+ * n >= 1 blocks (VC_ERR_SHAPE otherwise); the usual NULL / alignment checks. Not on the
+ * attention path: it exists so that the error bound assumed for FP8 scores can be measured. */
+vc_status vc_fp8_score_product(const uint8_t *a, const uint8_t *bm, const float *c_in, float *out, int32_t n,
+                               void *stream);
 
 /* Static description of a status code. */
 const char *vc_status_str(vc_status s);

@@ -86,6 +86,8 @@ def lib():
         L.vc_attn_forward_codes.restype = C.c_int
         L.vc_attn_forward_codes.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.POINTER(Prepped), C.c_void_p,
                                             C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.vc_fp8_score_product.restype = C.c_int
+        L.vc_fp8_score_product.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p]
         L.vc_opts_default.argtypes = [C.POINTER(Opts)]
         L.vc_group_opts_default.argtypes = [C.POINTER(GroupOpts)]
         _lib = L
@@ -209,6 +211,13 @@ def vc_attn_forward_codes(shape, opts, inp: PreppedBuffers, q_perm, O, p_codes, 
     _check("vc_attn_forward_codes", lib().vc_attn_forward_codes(C.byref(shape), C.byref(opts), C.byref(st),
                                                                 _ptr(q_perm), _ptr(O), _ptr(p_codes), nbytes,
                                                                 _stream(stream)))
+
+
+def vc_fp8_score_product(a, b, c_in, out, stream=None):
+    """a, b: uint8 E4M3 bytes [n, 32, 128]; c_in, out: fp32 [n, 32, 32] (device tensors)."""
+    n = a.shape[0]
+    _check("vc_fp8_score_product", lib().vc_fp8_score_product(_ptr(a), _ptr(b), _ptr(c_in), _ptr(out), n,
+                                                              _stream(stream)))
 
 
 class Attention:

@@ -34,7 +34,9 @@ vc_status check_opts(const vc_opts* o) {
   const int32_t flags[4] = {o->rope, o->hadamard, o->smooth_k, o->smooth_v};
   for (int32_t f : flags)
     if (f != 0 && f != 1) return VC_ERR_UNSUPPORTED;
-  if (!std::isfinite(o->sm_scale) || o->sm_scale < 0.f || !std::isfinite(o->beta)) return VC_ERR_UNSUPPORTED;
+  if (!std::isfinite(o->sm_scale) || o->sm_scale < 0.f) return VC_ERR_UNSUPPORTED;
+  // -1 <= beta <= 0 (NaN fails): the row maximum's ExpCast code stays in [119, 120]
+  if (!(o->beta >= -1.f && o->beta <= 0.f)) return VC_ERR_UNSUPPORTED;
   return VC_OK;
 }
 
@@ -311,6 +313,14 @@ vc_status vc_attn_forward_codes(const vc_shape* shape, const vc_opts* opts, cons
   const size_t need = (size_t)shape->B * shape->H * shape->N * ((size_t)blocks_of(shape->N, 128) * 128);
   if (p_codes_bytes < need) return VC_ERR_WORKSPACE;
   return attn_forward(shape, opts, in, q_perm, O, p_codes, stream);
+}
+
+vc_status vc_fp8_score_product(const uint8_t* a, const uint8_t* b, const float* c_in, float* out, int32_t n,
+                               void* stream) {
+  if (!a || !b || !c_in || !out) return VC_ERR_NULL;
+  if (n < 1) return VC_ERR_SHAPE;
+  if (!aligned16(a) || !aligned16(b) || !aligned16(c_in) || !aligned16(out)) return VC_ERR_ALIGN;
+  return hip_status(vc::launch_fp8_score_product(a, b, c_in, out, n, static_cast<hipStream_t>(stream)));
 }
 
 const char* vc_status_str(vc_status s) {

@@ -184,6 +184,25 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
+// The clip of eq. direct-fp8 at code 120. The byte conversion saturates only at 255, and the code
+// of the tile's largest score is the fma of s a - m' <= 2^-1 ulp(m') with fl(cbias - 8m'): with
+// cbias = fl(120 + beta) <= 120 (-1 <= beta <= 0) and |m'| < 2^16 (log2 units) that is at most
+// 120 + 2^-5 + 2^-5 before the rounding to an integer, so no code exceeds 120. A wave whose row
+// maxima reach 2^16 clips its codes bytewise (a branch that scores of such size take).
+constexpr float WIDE_MAX = 65536.f;
+__device__ __forceinline__ void clip_codes(v8i (&pn)[2]) {
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const uint32_t u = (uint32_t)pn[kc][w];
+      uint32_t r = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) r |= min((u >> (8 * b)) & 0xffu, 120u) << (8 * b);
+      pn[kc][w] = (int)r;
+    }
+}
+
 // DUMP: also write the probability codes of every tile to a.p_codes (a debugging variant; the
 // stores wait for all copies in flight, so it runs unpipelined)
 template <int PMODE, int QKF, bool DUMP>
@@ -473,6 +492,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
         }
         pn[kb >> 1][4 * (kb & 1) + d4] = (int)w;
       }
+    if (PMODE == 0 && __builtin_amdgcn_ballot_w64(fabsf(m_new) >= WIDE_MAX)) clip_codes(pn);
     if (decltype(LASTC)::value) clear_padded(pn, kh, a.N - t * BLK);
   };
 
@@ -671,6 +691,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     pin(a8);
     pin(bias);
     pin(m_new);
+    const bool wide = PMODE == 0 && __builtin_amdgcn_ballot_w64(fabsf(m_new) >= WIDE_MAX);
     hook(1);
     fence();
     // R3: row sum and value products 4, 5; operands 6, 7; key operands of block 0; codes of block 0
@@ -722,6 +743,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
       l_run *= alpha_p;
     }
     m_run = m_new;
+    if (wide) clip_codes(pn);
     pc[0] = pn[0];
     pc[1] = pn[1];
     end_iter(cp ? 2 : 0);
@@ -811,6 +833,35 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
         *reinterpret_cast<uint2*>(orow + c0) = make_uint2(w0, w1);
       }
   }
+}
+
+// The FP8 score product on caller data (vc_fp8_score_product): one wave per 32x32 block, the two
+// chained 32x32x64 instructions of the scores of a 32-key block (A = rows of a, B = rows of b),
+// from the accumulator c_in. Operand lane l holds row l % 32, channels 64m + 32(l / 32) .. + 31.
+__global__ __launch_bounds__(64) void fp8_score_product(const uint8_t* a, const uint8_t* b, const float* c_in,
+                                                        float* out) {
+  const int lane = threadIdx.x, row = lane & 31, half = lane >> 5;
+  const size_t blk = blockIdx.x;
+  const uint8_t* ar = a + (blk * 32 + row) * D + 32 * half;
+  const uint8_t* br = b + (blk * 32 + row) * D + 32 * half;
+  auto op = [](const uint8_t* p) -> v8i {
+    const u4 lo = *reinterpret_cast<const u4*>(p), hi = *reinterpret_cast<const u4*>(p + 16);
+    return v8i{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  };
+  // C register r of lane l: row 8(r/4) + 4(l/32) + r%4, column l%32
+  v16f acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = c_in[(blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3)) * 32 + row];
+  acc = mfma_f8(op(ar), op(br), acc);
+  acc = mfma_f8(op(ar + 64), op(br + 64), acc);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) out[(blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3)) * 32 + row] = acc[r];
+}
+
+hipError_t launch_fp8_score_product(const uint8_t* a, const uint8_t* b, const float* c_in, float* out, int n,
+                                    hipStream_t s) {
+  fp8_score_product<<<n, 64, 0, s>>>(a, b, c_in, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s) {

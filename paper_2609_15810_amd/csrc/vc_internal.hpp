@@ -67,5 +67,7 @@ struct GroupArgs {
 hipError_t launch_prep(const PrepArgs& a, int BH, hipStream_t s);
 hipError_t launch_forward(const FwdArgs& a, int BH, hipStream_t s);
 hipError_t launch_group(const GroupArgs& a, int BH, hipStream_t s);
+hipError_t launch_fp8_score_product(const uint8_t* a, const uint8_t* b, const float* c_in, float* out, int n,
+                                    hipStream_t s);
 
 }  // namespace vc

@@ -116,6 +116,37 @@ def test_forward_and_group_validation(L):
     assert L.vc_attn_group(C.byref(shape()), C.byref(g), FAKE, None, FAKE, FAKE, None, None, 0, None) == 3
 
 
+def test_option_limits(L):
+    """The documented limits are accepted and the first value past them is rejected: k-means
+    k <= 64 (and <= N), ExpCast shift -1 <= beta <= 0."""
+    s = shape()
+    for k, ok in ((1, True), (64, True), (65, False), (0, False)):
+        g = vc.make_group_opts(k=k)
+        assert (vc.workspace_size(s, None, g) > 0) == ok, k
+        # past the option checks a 16-byte workspace is too small (4); k out of range is 3
+        st = L.vc_attn_group(C.byref(s), C.byref(g), FAKE, FAKE, FAKE, FAKE, None, FAKE, 16, None)
+        assert st == (4 if ok else 3), (k, st)
+    tiny = vc.make_shape(1, 1, (1, 1, 40))
+    assert vc.workspace_size(tiny, None, vc.make_group_opts(k=40)) > 0
+    assert vc.workspace_size(tiny, None, vc.make_group_opts(k=41)) == 0     # k > N
+    for beta, ok in ((-0.35, True), (0.0, True), (-1.0, True), (1e-7, False), (-1.0001, False),
+                     (float("nan"), False), (float("inf"), False)):
+        o = vc.make_opts(beta=beta)
+        assert (vc.workspace_size(s, o, None) > 0) == ok, beta
+        assert prep_call(L, s, o, ws_bytes=16) == (4 if ok else 3), beta
+        P = vc.Prepped(*([FAKE] * 8))
+        st = L.vc_attn_forward(C.byref(s), C.byref(o), C.byref(P), None, None, None)
+        assert st == (1 if ok else 3), (beta, st)        # past the option check: O is NULL
+
+
+def test_fp8_score_product_validation(L):
+    f = L.vc_fp8_score_product
+    assert f(None, FAKE, FAKE, FAKE, 1, None) == 1
+    assert f(FAKE, FAKE, FAKE, None, 1, None) == 1
+    assert f(FAKE, FAKE, FAKE, FAKE, 0, None) == 2
+    assert f(FAKE, FAKE + 4, FAKE, FAKE, 1, None) == 5
+
+
 def test_workspace_size(L):
     s = vc.make_shape(1, 12, (21, 39, 40))
     o, g = vc.make_opts(), vc.make_group_opts()

@@ -100,7 +100,7 @@ def test_expcast_int8_codes_tile_counts(N):
     assert np.array_equal(O1, O2)
 
 
-@pytest.mark.parametrize("sm_scale,beta", [(0.05, -0.35), (0.125, 0.0), (0.0625, -0.5)])
+@pytest.mark.parametrize("sm_scale,beta", [(0.05, -0.35), (0.125, 0.0), (0.0625, -0.5), (0.0625, -1.0)])
 def test_expcast_int8_codes_softmax_scale_and_beta(sm_scale, beta):
     """Non-default softmax scale and ExpCast shift: codes bit-exact and the output within the
     tolerance of the oracle's pipeline with the same options."""
@@ -114,6 +114,30 @@ def test_expcast_int8_codes_softmax_scale_and_beta(sm_scale, beta):
     ref = oracle.attention(pp, rows, sm_scale=sm_scale, beta=beta)
     check_output(S.bits_to_f32(O2.view(np.uint16)).reshape(2, 1000, 128).astype(np.float64), ref,
                  f"sm_scale={sm_scale} beta={beta}")
+    assert np.array_equal(O1, O2)
+
+
+@pytest.mark.parametrize("sigma,beta", [(40.0, 0.0), (200.0, 0.0), (200.0, -0.35)])
+def test_expcast_int8_codes_huge_scores(sigma, beta):
+    """Scores whose running maximum exceeds 2^16 in log2 units (inputs of standard deviation
+    sigma, softmax scale 1): the fma that forms the code of a tile's largest score can then land
+    above 120.5, and the kernel's bytewise clip to 120 (eq. direct-fp8) must reproduce the
+    oracle's codes bit for bit; the output stays within the tolerance."""
+    rng = np.random.default_rng(int(sigma) + 7)
+    N = 700
+    Q = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * sigma).astype(np.float32))
+    K = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * sigma).astype(np.float32))
+    V = S.bf16_bits(rng.standard_normal((1, 2, N, 128)).astype(np.float32))
+    grid, perm = (1, 7, 100), S.random_perm(N, 8, 1, 2)
+    g, O1, O2 = gpu_codes(Q, K, V, grid, perm, sm_scale=1.0, beta=beta)
+    pp = oracle_pp(Q, K, V, grid, perm)
+    rows = np.arange(N)
+    o = oracle.attention_codes(pp, rows, sm_scale=1.0, beta=beta)
+    assert_codes_equal(g, o, rows, f"sigma={sigma} beta={beta}")
+    assert o.max() <= 120
+    ref = oracle.attention(pp, rows, sm_scale=1.0, beta=beta)
+    check_output(S.bits_to_f32(O2.view(np.uint16)).reshape(2, N, 128).astype(np.float64), ref,
+                 f"sigma={sigma} beta={beta}")
     assert np.array_equal(O1, O2)
 
 

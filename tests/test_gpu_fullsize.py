@@ -2,7 +2,9 @@
 
 * 32760-token layer (B=1, H=12, 21x39x40 grid): k-means grouping, preprocessing codes on all heads
   bit-exact; attention on sampled query rows (first, middle and the ragged last query block of
-  every head) within the tolerance.
+  every head) and on every row of one head within the tolerance.
+* Every output element of every call here is checked written and finite (the output buffer is
+  pre-filled with a NaN sentinel).
 * 75600-token layer (B=1, H=40, 21x60x60 grid): the same on all heads for grouping and codes,
   attention on sampled rows of a few heads; then a drifted call (inputs + 0.05 N(0,1)) reusing the
   permutation of the first call.
@@ -35,6 +37,19 @@ def log(msg):
     print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
 
 
+NAN_BF16 = 0x7FC0   # a quiet NaN in bf16: every element the kernel leaves unwritten stays NaN
+
+
+def sentinel_output(B, H, N):
+    return torch.full((B, H, N, 128), NAN_BF16, dtype=torch.int16, device="cuda")
+
+
+def assert_all_written(o, tag):
+    """Every element of O (pre-filled with the NaN sentinel) was written and is finite."""
+    bad = ~np.isfinite(o)
+    assert not bad.any(), f"{tag}: {int(bad.sum())} output elements unwritten or not finite, first {np.argwhere(bad)[:3].tolist()}"
+
+
 def run_gpu(name, Q, K, V, A=None, regroup=True):
     w = S.WORKLOADS[name]
     if A is None:
@@ -43,10 +58,12 @@ def run_gpu(name, Q, K, V, A=None, regroup=True):
     if regroup:
         A.group(Vd)
     A.prep(Qd, Kd, Vd)
-    O = torch.empty((w.B, w.H, w.N, 128), dtype=torch.int16, device="cuda")
+    O = sentinel_output(w.B, w.H, w.N)
     A.forward(O)
     torch.cuda.synchronize()
-    return A, S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(w.B * w.H, w.N, 128).astype(np.float64)
+    o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(w.B * w.H, w.N, 128).astype(np.float64)
+    assert_all_written(o, name)
+    return A, o
 
 
 def host_prepped(A):
@@ -82,6 +99,10 @@ def test_dit_small_full():
     log(f"oracle attention on {rows.size} rows x {w.H} heads")
     ref = oracle.attention(pp, rows)
     check_output(o[:, rows], ref, name)
+    h = 5
+    log(f"oracle attention on all {w.N} rows (all {(w.N + 127) // 128} query blocks) of head {h}")
+    ref = oracle.attention(pp, np.arange(w.N, dtype=np.int32), bh=[h])
+    check_output(o[h:h + 1], ref, f"{name} head {h} all rows")
 
 
 @pytest.mark.timeout(1200)
@@ -121,10 +142,12 @@ def test_dit_large_full_and_drift():
 
 def run_gpu_sub(A, Q, K, V, w):
     A.prep(dev16(Q), dev16(K), dev16(V))
-    O = torch.empty((1, Q.shape[1], w.N, 128), dtype=torch.int16, device="cuda")
+    O = sentinel_output(1, Q.shape[1], w.N)
     A.forward(O)
     torch.cuda.synchronize()
-    return A, S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(Q.shape[1], w.N, 128).astype(np.float64)
+    o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(Q.shape[1], w.N, 128).astype(np.float64)
+    assert_all_written(o, "sub-call")
+    return A, o
 
 
 @pytest.mark.timeout(900)
@@ -148,10 +171,11 @@ def test_loop_slice_warm_regroup():
     assert np.array_equal(A.perm.cpu().numpy(), g4["perm"])
     assert np.array_equal(f32_bits(A.centroids.cpu().numpy()), f32_bits(g4["centroids"]))
     A.prep(dev16(Q4), dev16(K4), dev16(V4))
-    O = torch.empty((1, len(heads), w.N, 128), dtype=torch.int16, device="cuda")
+    O = sentinel_output(1, len(heads), w.N)
     A.forward(O)
     torch.cuda.synchronize()
     o = S.bits_to_f32(O.cpu().numpy().view(np.uint16)).reshape(len(heads), w.N, 128).astype(np.float64)
+    assert_all_written(o, "loop call 4")
     pp = oracle.prep(Q4, K4, V4, w.grid, perm=g4["perm"])
     assert_prep_equal(host_prepped(A), pp, "loop call 4")
     rows = sample_rows(w.N)
