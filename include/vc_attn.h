@@ -210,6 +210,21 @@ vc_status vc_attn_prep(const vc_shape *shape, const vc_opts *opts, const uint16_
                        const int32_t *q_perm, const float *rope_cos, const float *rope_sin,
                        const vc_prepped *out, void *ws, size_t ws_bytes, void *stream);
 
+/* vc_attn_prep for callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): the same kernels and results, with the
+ * preprocessing workspace taken from a static device array of 32 MiB that the library holds on
+ * each GPU it runs on until the process ends, instead of a caller buffer. The call itself allocates
+ * nothing (no hipMalloc, no allocating library routine); the first call on a GPU looks up that
+ * GPU's copy of the array. Arguments and errors as vc_attn_prep, without ws / ws_bytes; shapes
+ * whose preprocessing workspace, vc_attn_workspace_size(shape, opts, NULL), exceeds 32 MiB
+ * (33554432 bytes; B * H * ceil(N / 128) up to about 32000) return VC_ERR_WORKSPACE. Every call on
+ * a GPU shares that GPU's array: calls that overlap in time on one GPU (different streams, or
+ * different threads) race and must be serialized by the caller. */
+vc_status vc_attn_prep_noalloc(const vc_shape *shape, const vc_opts *opts, const uint16_t *Q,
+                               const uint16_t *K, const uint16_t *V, const int32_t *perm,
+                               const int32_t *q_perm, const float *rope_cos, const float *rope_sin,
+                               const vc_prepped *out, void *stream);
+
 /* Attention kernel (Sec. 3.1 eq. tiled-low-bit-attention with Sec. 3.2 eq. vc-online-update and
  * Sec. 3.3 eq. direct-fp8): INT8 Q K'^T on the matrix cores, running row maximum per 128-key
  * tile (tiles in ascending order), 8-bit P (ExpCast-FP8 or exp-then-cast), FP8 P R_hat on the

@@ -80,6 +80,10 @@ def lib():
         L.vc_attn_prep.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Prepped),
                                    C.c_void_p, C.c_size_t, C.c_void_p]
+        L.vc_attn_prep_noalloc.restype = C.c_int
+        L.vc_attn_prep_noalloc.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.c_void_p, C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(Prepped),
+                                           C.c_void_p]
         L.vc_attn_forward.restype = C.c_int
         L.vc_attn_forward.argtypes = [C.POINTER(Shape), C.POINTER(Opts), C.POINTER(Prepped), C.c_void_p,
                                       C.c_void_p, C.c_void_p]
@@ -197,6 +201,13 @@ def vc_attn_prep(shape, opts, Q, K, V, perm, q_perm, rope_cos, rope_sin, out: Pr
     _check("vc_attn_prep", lib().vc_attn_prep(C.byref(shape), C.byref(opts), _ptr(Q), _ptr(K), _ptr(V), _ptr(perm),
                                               _ptr(q_perm), _ptr(rope_cos), _ptr(rope_sin), C.byref(st), _ptr(ws),
                                               ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def vc_attn_prep_noalloc(shape, opts, Q, K, V, perm, q_perm, rope_cos, rope_sin, out: PreppedBuffers, stream=None):
+    st = out.as_struct()
+    _check("vc_attn_prep_noalloc", lib().vc_attn_prep_noalloc(C.byref(shape), C.byref(opts), _ptr(Q), _ptr(K), _ptr(V),
+                                                              _ptr(perm), _ptr(q_perm), _ptr(rope_cos), _ptr(rope_sin),
+                                                              C.byref(st), _stream(stream)))
 
 
 def vc_attn_forward(shape, opts, inp: PreppedBuffers, q_perm, O, stream=None):

@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "vc_attn.h"
 #include "vc_internal.hpp"
@@ -70,6 +71,33 @@ vc_status hip_status(hipError_t e) {
   if (e == hipSuccess) return VC_OK;
   g_last_hip = (int)e;
   return VC_ERR_HIP;
+}
+
+// Preprocessing workspace of vc_attn_prep_noalloc: one copy per GPU, held until the process ends.
+// In host code the name `scratch` is only a stand-in for the symbol; the device address of this
+// GPU's copy comes from hipGetSymbolAddress, once per device, and only that address is used.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+// Device address of the current GPU's scratch (looked up on the first call on that GPU).
+vc_status scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return VC_ERR_INTERNAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e);
+    if (!p) return VC_ERR_INTERNAL;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return VC_OK;
 }
 
 }  // namespace
@@ -193,13 +221,19 @@ vc_status vc_attn_group(const vc_shape* shape, const vc_group_opts* gopts, const
   return hip_status(vc::launch_group(a, (int)BH, static_cast<hipStream_t>(stream)));
 }
 
-vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_t* Q, const uint16_t* K,
-                       const uint16_t* V, const int32_t* perm, const int32_t* q_perm, const float* rope_cos,
-                       const float* rope_sin, const vc_prepped* out, void* ws, size_t ws_bytes, void* stream) {
+static vc_status prep_impl(const vc_shape* shape, const vc_opts* opts, const uint16_t* Q, const uint16_t* K,
+                           const uint16_t* V, const int32_t* perm, const int32_t* q_perm, const float* rope_cos,
+                           const float* rope_sin, const vc_prepped* out, void* ws, size_t ws_bytes, bool use_scratch,
+                           void* stream) {
   vc_status st = check_shape(shape);
   if (st != VC_OK) return st;
   if ((st = check_opts(opts)) != VC_OK) return st;
   if (!Q || !K || !V || !out) return VC_ERR_NULL;
+  if (use_scratch) {
+    // the workspace is this GPU's static scratch: refuse shapes that need more
+    ws_bytes = kScratchBytes;
+    if (prep_ws(shape) > ws_bytes) return VC_ERR_WORKSPACE;
+  }
   const bool mx = opts->qk_fmt == VC_QK_MXFP4;
   // the per-block fp32 scales (INT8) or the E8M0 scale bytes (MXFP4)
   const void* qsc = mx ? (const void*)out->q_mx_scale : (const void*)out->q_scale;
@@ -207,13 +241,15 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   if (!out->q || !qsc || !out->k || !ksc || !out->k_mean || !out->v || !out->v_scale || !out->v_mean)
     return VC_ERR_NULL;
   if (opts->rope && (!rope_cos || !rope_sin)) return VC_ERR_NULL;
-  if (!ws || ws_bytes < prep_ws(shape)) return VC_ERR_WORKSPACE;
-  const void* ptrs[] = {Q, K, V, out->q, qsc, out->k, ksc, out->k_mean, out->v, out->v_scale, out->v_mean, ws};
+  if (!use_scratch && (!ws || ws_bytes < prep_ws(shape))) return VC_ERR_WORKSPACE;
+  const void* ptrs[] = {Q, K, V, out->q, qsc, out->k, ksc, out->k_mean, out->v, out->v_scale, out->v_mean};
   for (const void* p : ptrs)
     if (!aligned16(p)) return VC_ERR_ALIGN;
   if ((perm && !aligned16(perm)) || (q_perm && !aligned16(q_perm)) || (rope_cos && !aligned16(rope_cos)) ||
-      (rope_sin && !aligned16(rope_sin)))
+      (rope_sin && !aligned16(rope_sin)) || (!use_scratch && !aligned16(ws)))
     return VC_ERR_ALIGN;
+  // the last step before launching: the validation above fails the same way with and without a GPU
+  if (use_scratch && (st = scratch_ptr(&ws)) != VC_OK) return st;
 
   vc::PrepArgs a{};
   const size_t BH = (size_t)shape->B * shape->H, T = blocks_of(shape->N, 128);
@@ -253,6 +289,18 @@ vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_
   a.q_mxs = out->q_mx_scale;
   a.k_mxs = out->k_mx_scale;
   return hip_status(vc::launch_prep(a, (int)BH, static_cast<hipStream_t>(stream)));
+}
+
+vc_status vc_attn_prep(const vc_shape* shape, const vc_opts* opts, const uint16_t* Q, const uint16_t* K,
+                       const uint16_t* V, const int32_t* perm, const int32_t* q_perm, const float* rope_cos,
+                       const float* rope_sin, const vc_prepped* out, void* ws, size_t ws_bytes, void* stream) {
+  return prep_impl(shape, opts, Q, K, V, perm, q_perm, rope_cos, rope_sin, out, ws, ws_bytes, false, stream);
+}
+
+vc_status vc_attn_prep_noalloc(const vc_shape* shape, const vc_opts* opts, const uint16_t* Q, const uint16_t* K,
+                               const uint16_t* V, const int32_t* perm, const int32_t* q_perm, const float* rope_cos,
+                               const float* rope_sin, const vc_prepped* out, void* stream) {
+  return prep_impl(shape, opts, Q, K, V, perm, q_perm, rope_cos, rope_sin, out, nullptr, 0, true, stream);
 }
 
 static vc_status attn_forward(const vc_shape* shape, const vc_opts* opts, const vc_prepped* in, const int32_t* q_perm,

@@ -139,6 +139,27 @@ def test_option_limits(L):
         assert st == (1 if ok else 3), (beta, st)        # past the option check: O is NULL
 
 
+def test_prep_noalloc_validation(L):
+    """vc_attn_prep_noalloc validates like vc_attn_prep, and refuses shapes whose preprocessing
+    workspace exceeds its 32 MiB static scratch, before touching any GPU."""
+    o = vc.make_opts()
+    P = vc.Prepped(*([FAKE] * 8))
+    f = lambda s, o, P: L.vc_attn_prep_noalloc(C.byref(s), C.byref(o), FAKE, FAKE, FAKE, None, None, FAKE, FAKE,
+                                               C.byref(P), None)
+    assert f(shape(d=64), o, P) == 2
+    bad = vc.make_opts(beta=0.5)
+    assert f(shape(), bad, P) == 3
+    big = vc.make_shape(1, 64, (21, 60, 60))           # 64 * 591 blocks of partials: over 32 MiB
+    assert vc.workspace_size(big, o, None) > (32 << 20)
+    assert f(big, o, P) == 4
+    ok = vc.make_shape(1, 40, (21, 60, 60))            # the 75600-token, 40-head layer fits
+    assert vc.workspace_size(ok, o, None) <= (32 << 20)
+    Pn = vc.Prepped(*([FAKE] * 8)); Pn.v = None
+    assert f(ok, o, Pn) == 1
+    Pa = vc.Prepped(*([FAKE] * 8)); Pa.q = FAKE + 4
+    assert f(ok, o, Pa) == 5
+
+
 def test_fp8_score_product_validation(L):
     f = L.vc_fp8_score_product
     assert f(None, FAKE, FAKE, FAKE, 1, None) == 1
