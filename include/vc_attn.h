@@ -232,7 +232,11 @@ vc_status vc_attn_prep_noalloc(const vc_shape *shape, const vc_opts *opts, const
  *   in     : operands written by vc_attn_prep with the same shape and opts.
  *   q_perm : the q_perm given to vc_attn_prep (output row i is written to token q_perm[i]);
  *            NULL = query order.
- *   O      : bf16 bits [B, H, N, 128], token order. */
+ *   O      : bf16 bits [B, H, N, 128], token order.
+ * Domain: with p_mode = VC_P_EXPCAST, a query row whose running maximum score in log2 units
+ * (sm_scale * log2(e) * q.k of the quantized operands) reaches 2^27 in magnitude, i.e. softmax
+ * logits beyond about 9.3e7, is outside the supported domain: its output row is written as NaN.
+ * Every other row is the method's result (codes exactly those of eq. direct-fp8). */
 vc_status vc_attn_forward(const vc_shape *shape, const vc_opts *opts, const vc_prepped *in,
                           const int32_t *q_perm, uint16_t *O, void *stream);
 

@@ -80,6 +80,7 @@ __device__ __forceinline__ void wait_pairs(int n) {
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
@@ -184,12 +185,17 @@ __device__ __forceinline__ void clear_padded(v8i (&pop)[2], int kh, int kvalid) 
     }
 }
 
-// The clip of eq. direct-fp8 at code 120. The byte conversion saturates only at 255, and the code
-// of the tile's largest score is the fma of s a - m' <= 2^-1 ulp(m') with fl(cbias - 8m'): with
-// cbias = fl(120 + beta) <= 120 (-1 <= beta <= 0) and |m'| < 2^16 (log2 units) that is at most
-// 120 + 2^-5 + 2^-5 before the rounding to an integer, so no code exceeds 120. A wave whose row
-// maxima reach 2^16 clips its codes bytewise (a branch that scores of such size take).
+// The clip of eq. direct-fp8 at code 120. The fma that forms the code of a score s <= M (the
+// tile's largest) is at most cbias + 8(M a - fl(M a)) + |fl(cbias - 8m') - (cbias - 8m')|
+// <= cbias + 4 ulp(m') + ulp(fl(cbias - 8m')) / 2 with cbias = fl(120 + beta) <= 120
+// (-1 <= beta <= 0). For |m'| < 2^16 (log2 units) that is below 120 + 2^-4, so no code exceeds
+// 120; a wave whose row maxima reach 2^16 clips its codes bytewise (a branch that scores of such
+// size take). For |m'| < 2^27 it is below 217, so the codes still fit the byte the fp16
+// conversion leaves (below 256) and the clip restores eq. direct-fp8. A row whose running
+// maximum reaches 2^27 (the first or the last tile's: the running maximum is monotone) is
+// outside that domain and its output is written as NaN.
 constexpr float WIDE_MAX = 65536.f;
+constexpr float DOMAIN_MAX = 134217728.f;
 __device__ __forceinline__ void clip_codes(v8i (&pn)[2]) {
 #pragma unroll
   for (int kc = 0; kc < 2; ++kc)
@@ -224,6 +230,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   __shared__ __attribute__((aligned(16))) uint16_t ub[2][2][D][8];
   __shared__ __attribute__((aligned(16))) float2 rm[NW][8][32];
   __shared__ float svs[D], inv_svs[D];
+  __shared__ float m_first[NW][32];  // each query's running maximum after tile 0
 
   // The dispatcher deals workgroups to the XCDs round-robin by linear id; the remap (a bijection
   // when the count divides evenly) gives each XCD a contiguous range of (head, query tile) pairs,
@@ -633,15 +640,23 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
       }
     };
     v8i pn[2];
-    float a8 = 0.f, bias = 0.f, a_s = 0.f, m_new = 0.f;
+    float a8t = 0.f, bt = 0.f, a_s = 0.f, m_new = 0.f;
+    // codes of key block kb. ExpCast: the fma is evaluated scaled by 2^-24, which is exact
+    // (fl(2^-24 x) = 2^-24 fl(x)), with the clamp at 0 folded into it; below 2^-13 the fp16 spacing
+    // is 2^-24, so the fp16 conversion of each pair rounds to the nearest-even integer code and
+    // leaves it in the low bits, and one byte permute packs four (codes below 256: see WIDE_MAX)
     auto codes_kb = [&](int kb) __attribute__((always_inline)) {
 #pragma unroll
       for (int d4 = 0; d4 < 4; ++d4) {
         uint32_t w = 0;
         if (PMODE == 0) {
+          float z[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            w = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf((float)s[kb][4 * d4 + q], a8, bias), q, w);
+            z[q] = __builtin_amdgcn_fmed3f(__builtin_fmaf((float)s[kb][4 * d4 + q], a8t, bt), 0.f, 1.f);
+          const h2 lo = __builtin_convertvector((v2f){z[0], z[1]}, h2);
+          const h2 hi = __builtin_convertvector((v2f){z[2], z[3]}, h2);
+          w = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo), 0x06040200u);
         } else {
           float pe[4];
 #pragma unroll
@@ -685,11 +700,11 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     m_new = fmaxf(m_run, (float)mx * a_s);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     float alpha_p = alpha;
-    a8 = 8.f * a_s;
-    bias = a.cbias - 8.f * m_new;
+    a8t = a_s * 0x1p-21f;                                       // 2^-24 8a
+    bt = __builtin_fmaf(m_new, -0x1p-21f, a.cbias * 0x1p-24f);  // 2^-24 fl(cbias - 8m')
     pin(alpha_p);
-    pin(a8);
-    pin(bias);
+    pin(a8t);
+    pin(bt);
     pin(m_new);
     const bool wide = PMODE == 0 && __builtin_amdgcn_ballot_w64(fabsf(m_new) >= WIDE_MAX);
     hook(1);
@@ -765,6 +780,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
     if (T == 1) softmax(YES, 0, pc, alpha, m_new);
     else softmax(NO, 0, pc, alpha, m_new);
     m_run = m_new;
+    if (kh == 0) m_first[wave][col] = m_run;
   }
   if (t2) {
     if (T == 2) qk(YES, 1, kb1);
@@ -818,7 +834,9 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   // epilogue: O = A s_V / l, bf16, row q written to token q_perm[q] (or q)
   const int q = qt * NQ + wave * 32 + col;
   if (q < a.N) {
-    const float inv_l = 1.f / l_run;
+    // a row outside the domain of the fp16 code conversion is written as NaN
+    const bool out_of_domain = PMODE == 0 && (fabsf(m_first[wave][col]) >= DOMAIN_MAX || fabsf(m_run) >= DOMAIN_MAX);
+    const float inv_l = out_of_domain ? __builtin_nanf("") : 1.f / l_run;
     const int qo = a.q_perm ? clamp_index(a.q_perm[(size_t)bh * a.N + q], a.N) : q;
     uint16_t* orow = a.O + ((size_t)bh * a.N + qo) * D;
 #pragma unroll

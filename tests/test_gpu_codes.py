@@ -117,12 +117,12 @@ def test_expcast_int8_codes_softmax_scale_and_beta(sm_scale, beta):
     assert np.array_equal(O1, O2)
 
 
-@pytest.mark.parametrize("sigma,beta", [(40.0, 0.0), (200.0, 0.0), (200.0, -0.35)])
+@pytest.mark.parametrize("sigma,beta", [(40.0, 0.0), (200.0, 0.0), (200.0, -0.35), (1000.0, -0.35)])
 def test_expcast_int8_codes_huge_scores(sigma, beta):
-    """Scores whose running maximum exceeds 2^16 in log2 units (inputs of standard deviation
-    sigma, softmax scale 1): the fma that forms the code of a tile's largest score can then land
-    above 120.5, and the kernel's bytewise clip to 120 (eq. direct-fp8) must reproduce the
-    oracle's codes bit for bit; the output stays within the tolerance."""
+    """Scores whose running maximum lies between 2^16 and 2^27 in log2 units (inputs of standard
+    deviation sigma, softmax scale 1): the fma that forms the code of a tile's largest score can
+    then land above 120.5, and the kernel's bytewise clip to 120 (eq. direct-fp8) must reproduce
+    the oracle's codes bit for bit; the output stays within the tolerance."""
     rng = np.random.default_rng(int(sigma) + 7)
     N = 700
     Q = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * sigma).astype(np.float32))
@@ -132,12 +132,64 @@ def test_expcast_int8_codes_huge_scores(sigma, beta):
     g, O1, O2 = gpu_codes(Q, K, V, grid, perm, sm_scale=1.0, beta=beta)
     pp = oracle_pp(Q, K, V, grid, perm)
     rows = np.arange(N)
+    first, last = running_max_ends(pp, 0, rows, 1.0)
+    ext = np.maximum(np.abs(first), np.abs(last))
+    assert ext.max() >= 2.0 ** 16 and ext.max() < 2.0 ** 27, ext.max()
     o = oracle.attention_codes(pp, rows, sm_scale=1.0, beta=beta)
     assert_codes_equal(g, o, rows, f"sigma={sigma} beta={beta}")
     assert o.max() <= 120
     ref = oracle.attention(pp, rows, sm_scale=1.0, beta=beta)
     check_output(S.bits_to_f32(O2.view(np.uint16)).reshape(2, N, 128).astype(np.float64), ref,
                  f"sigma={sigma} beta={beta}")
+    assert np.array_equal(O1, O2)
+
+
+def running_max_ends(pp, h, rows, sm_scale):
+    """Each row's running maximum (log2 units, fp32 as the recurrence forms it) after the first and
+    after the last key tile, for head h of INT8 prepared operands."""
+    N = pp["N"]
+    T = (N + 127) // 128
+    q = pp["q"].reshape(-1, T * 128, 128)[h].astype(np.int64)
+    k = pp["k"].reshape(-1, T * 128, 128)[h, :N].astype(np.int64)
+    qs = pp["q_scale"].reshape(-1, T)[h]
+    ks = pp["k_scale"].reshape(-1, T)[h]
+    kappa = np.float32(sm_scale * np.log2(np.e) / (128.0 if pp["hadamard"] else 1.0))
+    first, last = np.zeros(len(rows)), np.zeros(len(rows))
+    for t, i in enumerate(rows):
+        acc = k @ q[i]
+        m = -np.inf
+        for j in range(T):
+            a = np.float32(np.float32(qs[i // 128] * ks[j]) * kappa)
+            m = max(m, float(np.float32(np.float32(acc[128 * j:128 * j + 128].max()) * a)))
+            if j == 0:
+                first[t] = m
+        last[t] = m
+    return first, last
+
+
+def test_expcast_out_of_domain_rows_are_nan():
+    """A row whose running maximum reaches 2^27 in log2 units (softmax logits beyond ~9e7) is
+    outside the domain of the kernel's code conversion and is written as NaN; a head of ordinary
+    scores in the same call is unaffected (codes bit-exact, output within the tolerance)."""
+    rng = np.random.default_rng(99)
+    N = 700
+    sig = np.array([3000.0, 1.0])[None, :, None, None]
+    Q = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * sig).astype(np.float32))
+    K = S.bf16_bits((rng.standard_normal((1, 2, N, 128)) * sig).astype(np.float32))
+    V = S.bf16_bits(rng.standard_normal((1, 2, N, 128)).astype(np.float32))
+    grid = (1, 7, 100)
+    g, O1, O2 = gpu_codes(Q, K, V, grid, sm_scale=1.0)
+    pp = oracle_pp(Q, K, V, grid)
+    rows = np.arange(N)
+    first, last = running_max_ends(pp, 0, rows, 1.0)
+    assert (np.maximum(np.abs(first), np.abs(last)) >= 2.0 ** 27).all()   # the premise: head 0 is out
+    f1, l1 = running_max_ends(pp, 1, rows, 1.0)
+    assert (np.maximum(np.abs(f1), np.abs(l1)) < 2.0 ** 16).all()        # head 1 is ordinary
+    o = S.bits_to_f32(O2.view(np.uint16)).reshape(2, N, 128).astype(np.float64)
+    assert np.isnan(o[0]).all()
+    codes = oracle.attention_codes(pp, rows, bh=[1], sm_scale=1.0)
+    assert_codes_equal(g[1:2], codes, rows, "ordinary head")
+    check_output(o[1:2], oracle.attention(pp, rows, bh=[1], sm_scale=1.0), "ordinary head")
     assert np.array_equal(O1, O2)
 
 
