@@ -22,6 +22,13 @@ same inputs and permutation, timed, and (with the CPU leg) both compared with ex
 exponentiate-then-cast) on the main layer and its permutation, attention timed per mode and (with
 the CPU leg) compared with exact fp64 attention.
 
+`ceiling`: the matrix-core ceiling measured on this GPU by the standalone probe
+(paper_2609_15810_amd/mfma_probe): sustained INT8 and FP8 product rates with random operands (the
+chip lowers its clock to stay in its power budget, so data sheet rates are not reached on real data),
+the attention kernel's own operation mix priced at those rates, and the vector work one wave issues
+under one product. `power_study`: the attention kernel on the same layer with all-zero inputs (the
+same instructions, no switching activity in the products) beside the real inputs.
+
 `--grouping-study` runs only the token-order study instead (see `grouping_study`), `--prep-ladder`
 only the preprocessing fusion ladder (see `prep_ladder`).
 
@@ -77,6 +84,57 @@ def measured_traffic():
     if c.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     return c.get("hbm_bytes_per_launch")
+
+
+PROBE = os.path.join(ROOT, "paper_2609_15810_amd", "mfma_probe")
+
+
+def measured_ceiling(B, H, N, attn_tops, d=128):
+    """Run the matrix-core probe and price the attention kernel's products at the measured rates.
+
+    Per 32 queries x 128 keys the kernel issues the INT8 score products (2 x 32 x 128 x d
+    operations), the FP8 value products (as many), the FP8 row-sum products (1/8 of those) and, once
+    per 8 tiles, the bf16 mean products (1/32 of the value products at half the FP8 rate)."""
+    import subprocess
+    if not os.path.exists(PROBE):
+        raise RuntimeError(f"{PROBE} is missing: build it with paper_2609_15810_amd/build.py")
+    r = subprocess.run([PROBE], capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        raise RuntimeError(f"mfma_probe failed ({r.returncode}): {r.stderr[-2000:]}")
+    p = json.loads(r.stdout.strip().splitlines()[-1])
+    r_i8 = p["rate"]["int8_32x32x32_random"]["tops"]
+    r_f8 = p["rate"]["fp8_32x32x64_random"]["tops"]
+    half = 2.0 * B * H * N * N * d
+    t = half / r_i8 + half * (1.0 + 1.0 / 8 + 1.0 / 16) / r_f8
+    mix = 2.0 * half / t
+    return {"probe": p, "int8_random_tops": r_i8, "fp8_random_tops": r_f8,
+            "attention_mix_ceiling_tops": mix, "attention_frac_of_mix_ceiling": attn_tops / mix,
+            "note": "effective TOPS (4 B H N^2 d per attention) the kernel's product mix reaches at the "
+                    "measured random-operand rates with no other work"}
+
+
+def power_study(vc, S, B, H, grid, reps=20):
+    """Attention on all-zero Q/K/V (same layer, same instructions; the grouping permutation from the
+    real V in both cases) beside the real inputs."""
+    import torch
+    w = S.WORKLOADS[WORKLOAD]
+    Q, K, V = S.make_qkv(WORKLOAD, seed=0)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    res = {}
+    for tag, zero in (("real", False), ("zero_inputs", True)):
+        A = vc.Attention(B, H, grid)
+        q, k, v = (np.zeros_like(x) for x in (Q, K, V)) if zero else (Q, K, V)
+        A.group(dev(V))
+        A.prep(dev(q), dev(k), dev(v))
+        O = torch.empty((B, H, w.N, 128), dtype=torch.int16, device="cuda")
+        for _ in range(2 * reps):
+            A.forward(O)
+        torch.cuda.synchronize()
+        ms = time_stages([lambda: A.forward(O)], reps)[0]
+        res[tag] = {"attn_ms": ms, "tops": 4.0 * B * H * w.N * w.N * 128 / (ms * 1e-3) / 1e12}
+        del A, O
+    res["zero_over_real_speedup"] = res["real"]["attn_ms"] / res["zero_inputs"]["attn_ms"]
+    return res
 
 
 def cpu_baseline(Q, K, V, grid, O_gpu, rows_per_head=1536):
@@ -732,6 +790,10 @@ def main():
         out["large_layer"] = large_layer(vc, S)
         print("[bench] 4-bit variant layer", file=sys.stderr, flush=True)
         out["mx4_layer"], mx4_sample = mx4_layer(vc, S)
+        print("[bench] attention on zero inputs", file=sys.stderr, flush=True)
+        out["power_study"] = power_study(vc, S, B, H, grid)
+        print("[bench] matrix-core ceiling probe", file=sys.stderr, flush=True)
+        out["ceiling"] = measured_ceiling(B, H, N, attn_tops)
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle sample", file=sys.stderr, flush=True)
         O_host = S.bits_to_f32(O.cpu().numpy().view(np.uint16))

@@ -1,4 +1,5 @@
-"""Build the HIP library libvcattn.so for gfx950 (hipcc), in-tree next to this file."""
+"""Build the HIP library libvcattn.so for gfx950 (hipcc), in-tree next to this file, and the
+standalone matrix-core probe mfma_probe (the measured ceilings bench.py reports beside the roofline)."""
 from __future__ import annotations
 
 import os
@@ -12,6 +13,7 @@ OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libvcattn.so")
 SOURCES = ["api.hip", "prep.hip", "forward.hip", "group.hip"]
 HEADERS = ["vc_common.hpp", "vc_internal.hpp"]
+PROBE = os.path.join(HERE, "mfma_probe")
 
 # -ffp-contract=off: every fp32 operation that decides a stored code is a single IEEE operation,
 # fused multiply-adds are written explicitly. Packed fp32 instructions are disabled.
@@ -29,11 +31,24 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _probe() -> str:
+    tmp = PROBE + ".tmp%d" % os.getpid()
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang",
+           "-packed-fp32-ops", os.path.join(CSRC, "mfma_probe.hip"), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for mfma_probe.hip:\n{r.stderr}")
+    os.replace(tmp, PROBE)
+    return PROBE
+
+
 def build() -> str:
-    """Compile every source and link the shared library (always rebuilds)."""
+    """Compile every source and link the shared library, and build the probe (always rebuilds)."""
     os.makedirs(OBJ, exist_ok=True)
-    with ThreadPoolExecutor(len(SOURCES)) as ex:
+    with ThreadPoolExecutor(len(SOURCES) + 1) as ex:
+        probe = ex.submit(_probe)
         objs = list(ex.map(_compile, SOURCES))
+        probe.result()
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
