@@ -89,12 +89,13 @@ def measured_traffic():
 PROBE = os.path.join(ROOT, "paper_2609_15810_amd", "mfma_probe")
 
 
-def measured_ceiling(B, H, N, attn_tops, d=128):
+def measured_ceiling(attn_tops, mx4_tops=None):
     """Run the matrix-core probe and price the attention kernel's products at the measured rates.
 
-    Per 32 queries x 128 keys the kernel issues the INT8 score products (2 x 32 x 128 x d
-    operations), the FP8 value products (as many), the FP8 row-sum products (1/8 of those) and, once
-    per 8 tiles, the bf16 mean products (1/32 of the value products at half the FP8 rate)."""
+    Per 32 queries x 128 keys the kernel issues the score products (2 x 32 x 128 x d operations;
+    INT8, or FP4 in the 4-bit variant), the FP8 value products (as many), the FP8 row-sum products
+    (1/8 of those) and, once per 8 tiles, the bf16 mean products (1/32 of the value products at half
+    the FP8 rate). Returned in effective TOPS of the metric (4 B H N^2 d per attention call)."""
     import subprocess
     if not os.path.exists(PROBE):
         raise RuntimeError(f"{PROBE} is missing: build it with paper_2609_15810_amd/build.py")
@@ -104,13 +105,18 @@ def measured_ceiling(B, H, N, attn_tops, d=128):
     p = json.loads(r.stdout.strip().splitlines()[-1])
     r_i8 = p["rate"]["int8_32x32x32_random"]["tops"]
     r_f8 = p["rate"]["fp8_32x32x64_random"]["tops"]
-    half = 2.0 * B * H * N * N * d
-    t = half / r_i8 + half * (1.0 + 1.0 / 8 + 1.0 / 16) / r_f8
-    mix = 2.0 * half / t
-    return {"probe": p, "int8_random_tops": r_i8, "fp8_random_tops": r_f8,
-            "attention_mix_ceiling_tops": mix, "attention_frac_of_mix_ceiling": attn_tops / mix,
-            "note": "effective TOPS (4 B H N^2 d per attention) the kernel's product mix reaches at the "
-                    "measured random-operand rates with no other work"}
+    r_f4 = p["rate"]["fp4_32x32x64_random"]["tops"]
+    rest = (1.0 + 1.0 / 8 + 1.0 / 16) / r_f8   # value, row-sum and mean products per score operation
+    mix = 2.0 / (1.0 / r_i8 + rest)
+    res = {"probe": p, "int8_random_tops": r_i8, "fp8_random_tops": r_f8, "fp4_random_tops": r_f4,
+           "attention_mix_ceiling_tops": mix, "attention_frac_of_mix_ceiling": attn_tops / mix,
+           "note": "effective TOPS (4 B H N^2 d per attention) the kernel's product mix reaches at the "
+                   "measured random-operand rates with no other work"}
+    if mx4_tops is not None:
+        mix4 = 2.0 / (1.0 / r_f4 + rest)
+        res["mxfp4_mix_ceiling_tops"] = mix4
+        res["mxfp4_frac_of_mix_ceiling"] = mx4_tops / mix4
+    return res
 
 
 def power_study(vc, S, B, H, grid, reps=20):
@@ -793,7 +799,7 @@ def main():
         print("[bench] attention on zero inputs", file=sys.stderr, flush=True)
         out["power_study"] = power_study(vc, S, B, H, grid)
         print("[bench] matrix-core ceiling probe", file=sys.stderr, flush=True)
-        out["ceiling"] = measured_ceiling(B, H, N, attn_tops)
+        out["ceiling"] = measured_ceiling(attn_tops, out["mx4_layer"]["mxfp4"]["attention_tops"])
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle sample", file=sys.stderr, flush=True)
         O_host = S.bits_to_f32(O.cpu().numpy().view(np.uint16))

@@ -1,8 +1,9 @@
 // Matrix-core limits of this GPU that bound the attention kernel, measured rather than taken from
 // the data sheet. Standalone program (no library code), printed as one JSON object.
 //
-// 1. Sustained rate and core clock of the two products the attention kernel is built from, INT8
-//    32x32x32 (scores) and FP8 32x32x64 (value products), four independent accumulator chains per
+// 1. Sustained rate and core clock of the products the attention kernel is built from, INT8
+//    32x32x32 (scores), FP8 32x32x64 (value products) and, for the 4-bit variant's scores, the
+//    scaled FP4 32x32x64 (E2M1 operands, unit E8M0 scales), four independent accumulator chains per
 //    wave, two waves per SIMD, every CU busy. Operands either constant or random bytes (xorshift
 //    per lane; FP8 bytes masked with 0x77 so no NaN encodings occur). The clock is the ratio of the
 //    shader clock counter (s_memtime) to the 100 MHz constant counter (s_memrealtime) over each
@@ -37,12 +38,18 @@ __device__ __forceinline__ v16i mm_i8(v4i a, v4i b, v16i c) {
 __device__ __forceinline__ v16f mm_f8(v8i a, v8i b, v16f c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
+// FP4 x FP4 (cbsz = blgp = 4: 32 E2M1 codes in the low four registers), E8M0 scales 127 (= 1)
+__device__ __forceinline__ v16f mm_f4(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, 0, 127, 0, 127);
+}
 
-// Part 1. F8: FP8 32x32x64 (else INT8 32x32x32); RND: random operands (else constant ones).
-// Each workgroup writes its lane sums to out[block * blockDim + thread] (so nothing is removed as
-// dead) and, from thread 0, its shader-clock and constant-clock spans to clk[2 block .. + 1].
-template <bool F8, bool RND>
+// Part 1. KIND 0: INT8 32x32x32, 1: FP8 32x32x64, 2: FP4 32x32x64; RND: random operands (else
+// constant ones; every E2M1 code is finite, so FP4 takes any byte). Each workgroup writes its lane
+// sums to out[block * blockDim + thread] (so nothing is removed as dead) and, from thread 0, its
+// shader-clock and constant-clock spans to clk[2 block .. + 1].
+template <int KIND, bool RND>
 __global__ __launch_bounds__(512) void rate(int iters, float* out, unsigned long long* clk) {
+  constexpr bool F8 = KIND == 1;
   const int l = threadIdx.x;
   const unsigned long long t0 = __builtin_readcyclecounter();
   const unsigned long long w0 = __builtin_amdgcn_s_memrealtime();
@@ -57,13 +64,14 @@ __global__ __launch_bounds__(512) void rate(int iters, float* out, unsigned long
   v8i r[4];
   for (int m = 0; m < 4; ++m) r[m] = v8i{word(), word(), word(), word(), word(), word(), word(), word()};
   float sum = 0.f;
-  if constexpr (F8) {
+  if constexpr (KIND == 1 || KIND == 2) {
+    auto mm = [](v8i a, v8i b, v16f c) { return KIND == 1 ? mm_f8(a, b, c) : mm_f4(a, b, c); };
     v16f c0 = {}, c1 = {}, c2 = {}, c3 = {};
     for (int i = 0; i < iters; ++i) {
-      c0 = mm_f8(r[0], r[1], c0);
-      c1 = mm_f8(r[2], r[3], c1);
-      c2 = mm_f8(r[1], r[2], c2);
-      c3 = mm_f8(r[3], r[0], c3);
+      c0 = mm(r[0], r[1], c0);
+      c1 = mm(r[2], r[3], c1);
+      c2 = mm(r[1], r[2], c2);
+      c3 = mm(r[3], r[0], c3);
     }
     for (int q = 0; q < 16; ++q) sum += c0[q] + c1[q] + c2[q] + c3[q];
   } else {
@@ -141,18 +149,24 @@ int main() {
   CHECK(hipEventCreate(&e1));
 
   std::printf("{\"cus\": %d, \"rate\": {", ncu);
-  struct Case { const char* name; bool f8, rnd; double ops; };
-  const Case cases[4] = {{"int8_32x32x32_constant", false, false, 32.0 * 32 * 32 * 2},
-                         {"int8_32x32x32_random", false, true, 32.0 * 32 * 32 * 2},
-                         {"fp8_32x32x64_constant", true, false, 32.0 * 32 * 64 * 2},
-                         {"fp8_32x32x64_random", true, true, 32.0 * 32 * 64 * 2}};
-  for (int c = 0; c < 4; ++c) {
-    const int iters = cases[c].f8 ? 2000 : 4000;
+  struct Case { const char* name; int kind; bool rnd; double ops; int iters; };
+  const Case cases[6] = {{"int8_32x32x32_constant", 0, false, 32.0 * 32 * 32 * 2, 4000},
+                         {"int8_32x32x32_random", 0, true, 32.0 * 32 * 32 * 2, 4000},
+                         {"fp8_32x32x64_constant", 1, false, 32.0 * 32 * 64 * 2, 2000},
+                         {"fp8_32x32x64_random", 1, true, 32.0 * 32 * 64 * 2, 2000},
+                         {"fp4_32x32x64_constant", 2, false, 32.0 * 32 * 64 * 2, 4000},
+                         {"fp4_32x32x64_random", 2, true, 32.0 * 32 * 64 * 2, 4000}};
+  for (int c = 0; c < 6; ++c) {
+    const int iters = cases[c].iters;
     auto launch = [&]() {
-      if (cases[c].f8 && cases[c].rnd) rate<true, true><<<nblk, 512>>>(iters, out, clk);
-      else if (cases[c].f8) rate<true, false><<<nblk, 512>>>(iters, out, clk);
-      else if (cases[c].rnd) rate<false, true><<<nblk, 512>>>(iters, out, clk);
-      else rate<false, false><<<nblk, 512>>>(iters, out, clk);
+      switch (c) {
+        case 0: rate<0, false><<<nblk, 512>>>(iters, out, clk); break;
+        case 1: rate<0, true><<<nblk, 512>>>(iters, out, clk); break;
+        case 2: rate<1, false><<<nblk, 512>>>(iters, out, clk); break;
+        case 3: rate<1, true><<<nblk, 512>>>(iters, out, clk); break;
+        case 4: rate<2, false><<<nblk, 512>>>(iters, out, clk); break;
+        default: rate<2, true><<<nblk, 512>>>(iters, out, clk); break;
+      }
     };
     float ms = 0.f;
     for (int rep = 0; rep < 4; ++rep) {  // the clock settles over the first launches; the last counts
