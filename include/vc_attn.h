@@ -84,7 +84,8 @@ enum { VC_P_EXPCAST = 0, VC_P_EXP_THEN_CAST = 1 };
  *   smooth_k : 1 = subtract the key channel mean (over the N tokens) before quantizing K.
  *   smooth_v : 1 = V-Smooth block demeaning (means restored in the attention kernel);
  *              0 = plain per-channel E4M3 V.
- *   sm_scale : softmax scale; 0 selects 1/sqrt(d).
+ *   sm_scale : softmax scale, >= 0 with sm_scale * log2(e) finite in fp32 (VC_ERR_UNSUPPORTED
+ *              otherwise); 0 selects 1/sqrt(d).
  *   beta     : ExpCast-FP8 centring constant (the method uses -0.35), -1 <= beta <= 0
  *              (VC_ERR_UNSUPPORTED otherwise). Sec. 3.3 derives the shift from the rounding
  *              error range [-0.689, 0]; inside [-1, 0] the row maximum's code stays in
@@ -180,7 +181,8 @@ size_t vc_attn_workspace_size(const vc_shape *shape, const vc_opts *opts, const 
  * cos/sin of pair i's angle pos * theta^(-2j/d_a) (j = i minus the axis' first pair; d_a = 44
  * for frames, 42 for rows and columns) when pair i belongs to that row's axis, else 1 / 0.
  * Angles are evaluated in fp64 and rounded once to fp32. Copy the tables to the device for
- * vc_attn_prep. Returns VC_ERR_NULL / VC_ERR_SHAPE on bad arguments. */
+ * vc_attn_prep. Returns VC_ERR_NULL on NULL tables, VC_ERR_SHAPE for a non-positive extent, a
+ * theta that is not finite and positive, or F + Ht + Wd >= 2^25 (the entry count must fit int). */
 vc_status vc_rope_tables(int32_t F, int32_t Ht, int32_t Wd, double theta, float *cos_t, float *sin_t);
 
 /* Value-guided grouping (Sec. 3.2, "Value-guided permutation"; grouping schedule Sec. 3.4).

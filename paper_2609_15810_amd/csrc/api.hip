@@ -22,7 +22,9 @@ inline int blocks_of(int n, int b) { return (n + b - 1) / b; }
 vc_status check_shape(const vc_shape* s) {
   if (!s) return VC_ERR_NULL;
   if (s->d != kD || s->B < 1 || s->H < 1 || s->N < 1 || s->F < 1 || s->Ht < 1 || s->Wd < 1) return VC_ERR_SHAPE;
-  if ((long long)s->F * s->Ht * s->Wd != s->N) return VC_ERR_SHAPE;
+  // F * Ht <= N < 2^31 before the last factor, so the product cannot overflow
+  const long long fh = (long long)s->F * s->Ht;
+  if (fh > s->N || fh * s->Wd != s->N) return VC_ERR_SHAPE;
   const long long T = blocks_of(s->N, 128);
   if ((long long)s->B * s->H * T * 128 * kD >= (1LL << 31)) return VC_ERR_SHAPE;
   return VC_OK;
@@ -35,7 +37,8 @@ vc_status check_opts(const vc_opts* o) {
   const int32_t flags[4] = {o->rope, o->hadamard, o->smooth_k, o->smooth_v};
   for (int32_t f : flags)
     if (f != 0 && f != 1) return VC_ERR_UNSUPPORTED;
-  if (!std::isfinite(o->sm_scale) || o->sm_scale < 0.f) return VC_ERR_UNSUPPORTED;
+  // the score scale sm_scale * log2(e) must be finite in fp32 (NaN fails)
+  if (!(o->sm_scale >= 0.f) || !std::isfinite(o->sm_scale * 1.4426950408889634f)) return VC_ERR_UNSUPPORTED;
   // -1 <= beta <= 0 (NaN fails): the row maximum's ExpCast code stays in [119, 120]
   if (!(o->beta >= -1.f && o->beta <= 0.f)) return VC_ERR_UNSUPPORTED;
   return VC_OK;
@@ -141,7 +144,9 @@ size_t vc_attn_workspace_size(const vc_shape* shape, const vc_opts* opts, const 
 
 vc_status vc_rope_tables(int32_t F, int32_t Ht, int32_t Wd, double theta, float* cos_t, float* sin_t) {
   if (!cos_t || !sin_t) return VC_ERR_NULL;
-  if (F < 1 || Ht < 1 || Wd < 1 || !(theta > 0.0)) return VC_ERR_SHAPE;
+  if (F < 1 || Ht < 1 || Wd < 1 || !(theta > 0.0) || !std::isfinite(theta)) return VC_ERR_SHAPE;
+  // the tables hold (F + Ht + Wd) x 64 entries each: refuse sizes whose entry count overflows int
+  if ((long long)F + Ht + Wd > (1LL << 31) / 64 - 1) return VC_ERR_SHAPE;
   const int rows = F + Ht + Wd;
   for (int r = 0; r < rows; ++r) {
     const int axis = r < F ? 0 : (r < F + Ht ? 1 : 2);

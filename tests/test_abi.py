@@ -139,6 +139,30 @@ def test_option_limits(L):
         assert st == (1 if ok else 3), (beta, st)        # past the option check: O is NULL
 
 
+def test_shape_and_scale_limits(L):
+    """Grid extents whose product overflows 64 bits, a softmax scale whose log2 form overflows
+    fp32, and rotary tables whose entry count overflows int are refused before any launch."""
+    o = vc.make_opts()
+    big = vc.make_shape(1, 1, (4, 16, 16))
+    big.F, big.Ht, big.Wd = 2**31 - 1, 2**31 - 1, 2**31 - 1     # N stays 1024
+    assert vc.workspace_size(big, o, None) == 0
+    assert prep_call(L, big, o) == 2
+    wrap = vc.make_shape(1, 1, (4, 16, 16))
+    wrap.F, wrap.Ht, wrap.Wd = 2**21, 2**21, 2**22              # product 2^64 wraps to 0 in 64 bits
+    assert prep_call(L, wrap, o) == 2
+    s = shape()
+    for sm, ok in ((0.0, True), (0.125, True), (1e38, True), (3e38, False), (-1e-9, False), (float("nan"), False),
+                   (float("inf"), False)):
+        oo = vc.make_opts(sm_scale=sm)
+        assert (vc.workspace_size(s, oo, None) > 0) == ok, sm
+        assert prep_call(L, s, oo, ws_bytes=16) == (4 if ok else 3), sm
+    buf = (C.c_float * (3 * 64))()
+    for F, Ht, Wd, theta, st in ((1, 1, 1, 1e4, 0), (0, 1, 1, 1e4, 2), (1, 1, 1, 0.0, 2),
+                                 (1, 1, 1, float("inf"), 2), (2**24, 2**24, 1, 1e4, 2)):
+        assert L.vc_rope_tables(F, Ht, Wd, C.c_double(theta), buf, buf) == st, (F, Ht, Wd, theta)
+    assert L.vc_rope_tables(1, 1, 1, C.c_double(1e4), None, buf) == 1
+
+
 def test_prep_noalloc_validation(L):
     """vc_attn_prep_noalloc validates like vc_attn_prep, and refuses shapes whose preprocessing
     workspace exceeds its 32 MiB static scratch, before touching any GPU."""
