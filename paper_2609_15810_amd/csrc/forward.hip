@@ -27,7 +27,7 @@
 // only in rows 0, 4, 8 and 12 (so that lane l receives r of its own query). Block means are
 // restored in batches of 8 tiles: (r_j, m_j) is kept in LDS, and every 8 tiles O^T += M^T R with
 // R_t = r_t 2^(m_t - m) is one bf16 matrix product pair (mu_t / s_V and R split into hi + lo bf16
-// parts, relative error ~2^-16). The rescale by alpha is skipped when no row maximum of the wave
+// parts, all four cross terms, relative error ~2^-16). The rescale by alpha is skipped when no row maximum of the wave
 // moved.
 //
 // Tiles go straight from memory into LDS (16 KB of K_hat, 16 KB of V_hat per tile, four buffers
@@ -80,6 +80,7 @@ __device__ __forceinline__ void wait_pairs(int n) {
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
@@ -365,23 +366,32 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(NW / 4, NW 
   float ksc = 0.f;  // scale of the K tile whose scores are in s
   float2* rm_q = &rm[wave][0][col];   // slot t at rm_q[32 t]
 
-  // O^T += M^T R for the tiles of chunk parity `par` whose slot is <= last_slot, R_t = r_t 2^(m_t - m)
+  // O^T += M^T R for the tiles of chunk parity `par` whose slot is <= last_slot, R_t = r_t 2^(m_t - m).
+  // k-slots 0..7 (lanes with kh = 0) carry R_hi = bf16(R), slots 8..15 (kh = 1) R_lo = bf16(R - R_hi)
+  // (R - R_hi is exact in fp32, and fma(-kh, R_hi, R) is R itself for kh = 0), against mu_hi in the
+  // first product and mu_lo in the second: the four cross terms of the two splits.
+  const float khf = (float)kh;
   auto flush_means = [&](int par, int last_slot) __attribute__((always_inline)) {
-    bf16x8 b;
+    float R[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       const float2 e = rm_q[32 * t];
-      const float R = t <= last_slot ? e.x * __builtin_amdgcn_exp2f(e.y - m_run) : 0.f;
-      const uint16_t hi = f32_to_bf16(R);
-      const uint16_t v = kh == 0 ? hi : f32_to_bf16(R - bf16_to_f32(hi));
-      b[t] = __builtin_bit_cast(__bf16, v);
+      R[t] = t <= last_slot ? e.x * __builtin_amdgcn_exp2f(e.y - m_run) : 0.f;
+    }
+    bf16x8 b;
+#pragma unroll
+    for (int t = 0; t < 8; t += 2) {
+      const v2f hi = __builtin_convertvector(__builtin_convertvector((v2f){R[t], R[t + 1]}, bf16x2), v2f);
+      const v2f part = {__builtin_fmaf(-khf, hi[0], R[t]), __builtin_fmaf(-khf, hi[1], R[t + 1])};
+      const bf16x2 v = __builtin_convertvector(part, bf16x2);
+      b[t] = v[0];
+      b[t + 1] = v[1];
     }
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
       const int c = 32 * db + col;
       const bf16x8 a_hi = *reinterpret_cast<const bf16x8*>(&ub[par][0][c][0]);
-      bf16x8 a_lo = *reinterpret_cast<const bf16x8*>(&ub[par][1][c][0]);
-      if (kh) a_lo = bf16x8{};
+      const bf16x8 a_lo = *reinterpret_cast<const bf16x8*>(&ub[par][1][c][0]);
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_hi, b, o[db], 0, 0, 0);
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_lo, b, o[db], 0, 0, 0);
     }
