@@ -20,15 +20,17 @@
 // thus run the value and score products of one wave while its vector ALU forms codes; the two
 // waves of a SIMD share both.
 //
-// Per score the vector ALU does one int-to-float conversion, one fp32 fma and one
-// round-to-nearest-even saturating byte conversion (the code is the one-rounding
-// fma(float(acc), 8a, fl(fl(120 + beta) - 8m')) of the method's fp32 formula), plus half a max3.
+// Per score the vector ALU does one int-to-float conversion, one fp32 fma (the code is the
+// one-rounding fma(float(acc), 8a, fl(fl(120 + beta) - 8m')) of the method's fp32 formula, evaluated
+// scaled by 2^-24 with the clamp at 0 folded in), half an fp16 pair conversion (which rounds to the
+// nearest-even integer code and leaves it in the low bits) and a quarter of a byte permute, plus
+// half a max3.
 // The probability row sum r_j is one FP8 16x16x128 product per 64 keys whose A operand holds ones
 // only in rows 0, 4, 8 and 12 (so that lane l receives r of its own query). Block means are
 // restored in batches of 8 tiles: (r_j, m_j) is kept in LDS, and every 8 tiles O^T += M^T R with
 // R_t = r_t 2^(m_t - m) is one bf16 matrix product pair (mu_t / s_V and R split into hi + lo bf16
-// parts, all four cross terms, relative error ~2^-16). The rescale by alpha is skipped when no row maximum of the wave
-// moved.
+// parts, all four cross terms, relative error ~2^-16). The rescale by alpha is skipped when no row
+// maximum of the wave moved.
 //
 // Tiles go straight from memory into LDS (16 KB of K_hat, 16 KB of V_hat per tile, four buffers
 // each), issued as asm so that the compiler adds no waits of its own: pair p = (K_{p+2}, V_p with
