@@ -107,7 +107,7 @@ def measured_ceiling(attn_tops, mx4_tops=None):
     import subprocess
     if not os.path.exists(PROBE):
         raise RuntimeError(f"{PROBE} is missing: build it with paper_2609_15810_amd/build.py")
-    r = subprocess.run([PROBE], capture_output=True, text=True, timeout=300)
+    r = subprocess.run([PROBE], capture_output=True, text=True, timeout=120)
     if r.returncode != 0:
         raise RuntimeError(f"mfma_probe failed ({r.returncode}): {r.stderr[-2000:]}")
     p = json.loads(r.stdout.strip().splitlines()[-1])
